@@ -27,9 +27,9 @@ Readings where the paper leaves a choice (each is also listed with the
 design notes of the repository):
 * the pivot m is the last point (Eq. (12) puts q in the last row/column);
 * CG starts at x = 0 and stops when r^T r <= eps^2 r0^T r0 (relative
-  residual eps, Sec. IV-B and IV-F); the residual is recomputed as
-  rhs - Q~ x every 50th iteration (Shewchuk's recommendation); CG also stops,
-  unconverged, after 20 iterations without a new smallest r^T r;
+  residual eps, Sec. IV-B and IV-F) or, unconverged, after max_iter
+  iterations (default N); the residual is recomputed as rhs - Q~ x every
+  50th iteration (Shewchuk's recommendation);
 * the decision label is +1 iff f(x) > 0.
 
 Pins (see tests/test_oracle_pins.py): every function here is checked against
@@ -45,7 +45,7 @@ import scipy.linalg as sla
 
 __all__ = [
     "KernelSpec", "kernel_matrix", "kernel_rows", "bordered_matrix",
-    "reduced_parts", "reduced_matrix", "reduced_rhs", "matvec_dense",
+    "reduced_parts", "reduced_matrix", "reduced_rows", "reduced_rhs", "matvec_dense",
     "matvec_rows", "solve_cholesky", "CGResult", "solve_cg", "recover",
     "train", "decision", "predict", "full_system_residual",
 ]
@@ -93,10 +93,22 @@ def _sqnorms(A):
     return np.einsum("ij,ij->i", A, A)
 
 
+def _gemm_nt(A, B):
+    """A @ B^T as a general matrix product.
+
+    numpy routes ``a @ a.T`` on one buffer to a symmetric rank-k update;
+    OpenBLAS 0.3.29's dsyrk returns wrong entries at n = 32768, d = 4096, so
+    aliasing operands are separated first.
+    """
+    if np.shares_memory(A, B):
+        B = B.copy()
+    return A @ B.T
+
+
 def kernel_rows(XA, XB, spec: KernelSpec):
     """k(a_i, b_j) for every row a_i of XA and b_j of XB (Sec. II-E)."""
     A, B = _f64(XA), _f64(XB)
-    G = A @ B.T
+    G = _gemm_nt(A, B)
     if spec.kind == "rbf":
         return _kernel_from_gram_(G, _sqnorms(A), _sqnorms(B), spec)
     return _kernel_from_gram_(G, None, None, spec)
@@ -115,21 +127,29 @@ def _mirror_upper_(G, bs: int = 1024):
     return G
 
 
-def kernel_matrix(X, spec: KernelSpec):
+def kernel_matrix(X, spec: KernelSpec, panel: int = 2048):
     """Symmetric n x n kernel matrix K_ij = k(x_i, x_j) (Sec. II-E).
 
-    The Gram matrix X X^T comes from a symmetric rank-k update (upper
-    triangle); the kernel map is applied and the upper triangle mirrored, so
-    K is exactly symmetric. One n x n buffer.
+    Row panels of the upper triangle come from general matrix products, get
+    the kernel map, and are mirrored, so K is exactly symmetric. One n x n
+    buffer plus one panel.
     """
-    A = np.asfortranarray(_f64(X))
-    # syrk with trans=0 on the column-major n x d matrix: upper triangle of A A^T
-    G = sla.blas.dsyrk(1.0, A, trans=0, lower=0)
+    A = _f64(X)
+    B = A.copy()                 # a separate operand: always a general product
+    n = A.shape[0]
     nrm = _sqnorms(A) if spec.kind == "rbf" else None
-    del A
-    _kernel_from_gram_(G, nrm, nrm, spec)
-    _mirror_upper_(G)
-    return G.T         # symmetric, so the row-major view holds the same matrix
+    K = np.empty((n, n))
+    for i0 in range(0, n, panel):
+        i1 = min(n, i0 + panel)
+        blk = A[i0:i1] @ B[i0:].T
+        if spec.kind == "rbf":
+            _kernel_from_gram_(blk, nrm[i0:i1], nrm[i0:], spec)
+        else:
+            _kernel_from_gram_(blk, None, None, spec)
+        K[i0:i1, i0:] = blk
+    del B
+    _mirror_upper_(K)
+    return K
 
 
 def bordered_matrix(X, spec: KernelSpec, C: float):
@@ -172,6 +192,26 @@ def reduced_matrix(X, spec: KernelSpec, C: float):
         Qt[i0:i1] -= q[i0:i1, None] + q[None, :]
         Qt[i0:i1] += Qmm
     return Qt, q, Qmm
+
+
+def reduced_rows(X, spec: KernelSpec, C: float, rows):
+    """Selected rows of Q~ (Eq. (13)) without forming the whole matrix.
+
+    Q~[r, j] = K[r, j] + delta_rj / C - (q_r + q_j) + Q_mm for j < N, with
+    q_j = k(x_j, x_m) and Q_mm = k(x_m, x_m) + 1/C as in Eq. (12).
+    """
+    X = _f64(X)
+    rows = np.asarray(rows, dtype=np.int64)
+    n = X.shape[0]
+    N = n - 1
+    xm = X[N:N + 1]
+    q = kernel_rows(X[:N], xm, spec)[:, 0]
+    Qmm = float(kernel_rows(xm, xm, spec)[0, 0]) + 1.0 / C
+    R = kernel_rows(X[rows], X[:N], spec)
+    R[np.arange(len(rows)), rows] += 1.0 / C
+    R -= q[rows][:, None] + q[None, :]
+    R += Qmm
+    return R
 
 
 def reduced_rhs(y):
@@ -227,7 +267,7 @@ class CGResult:
 
 
 def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
-             replace_every: int = 50, stall_iters: int = 20) -> CGResult:
+             replace_every: int = 50) -> CGResult:
     """Conjugate gradients for the SPD reduced system (Sec. III-B).
 
     matvec(v) returns Q~ v. Steps per iteration, in Shewchuk's notation:
@@ -248,8 +288,6 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
     nmv = 0
     if delta0 == 0.0:
         return CGResult(x, 0, True, 0.0, 0.0, 0, hist)
-    best = delta
-    since_best = 0
     converged = False
     it = 0
     while it < max_iter:
@@ -269,12 +307,6 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
         if delta <= eps * eps * delta0:
             converged = True
             break
-        if delta < best:
-            best, since_best = delta, 0
-        else:
-            since_best += 1
-            if since_best >= stall_iters:
-                break
         d = r + (delta / delta_old) * d
     true_res = float(np.linalg.norm(b - matvec(x)) / np.linalg.norm(b))
     return CGResult(x, it, converged, float(np.sqrt(delta / delta0)), true_res, nmv, hist)

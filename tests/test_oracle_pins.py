@@ -94,6 +94,18 @@ def test_reduced_matrix_is_PtQP(spec, C):
     assert np.allclose(mv, (ref @ p)[rows], rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("spec", SPECS, ids=lambda s: s.kind)
+def test_reduced_rows_match_PtQP(spec):
+    """Row panels of Q~ (used where the full matrix does not fit) equal P^T Q P."""
+    X, _ = small_problem(n=41, d=5)
+    n = X.shape[0]
+    M = O.bordered_matrix(X, spec, 0.3)
+    ref = P_matrix(n).T @ M[:n, :n] @ P_matrix(n)
+    rows = [0, 3, 17, 39]
+    R = O.reduced_rows(X, spec, 0.3, rows)
+    assert np.abs(R - ref[rows]).max() <= 1e-12 * max(1.0, np.abs(ref).max())
+
+
 def test_reduced_parts_partition():
     """Eq. (12): q is the last column of Q (without the last entry), Q_mm its corner."""
     X, _ = small_problem(n=12, d=3)
@@ -387,17 +399,13 @@ def test_cg_residual_replacement_and_max_iter():
     assert not short.converged and short.iterations == 3
 
 
-def test_cg_stall_guard():
-    """An affine (not linear) operator keeps CG from progressing: the stall rule ends it."""
+def test_cg_runs_to_max_iter_without_progress():
+    """An affine (not linear) operator keeps CG from converging: it ends at max_iter."""
     rng = np.random.default_rng(0)
     A = np.diag(np.linspace(1, 10, 30))
     z = rng.standard_normal(30)
-    res = O.solve_cg(lambda v: A @ v + 0.5 * z, np.ones(30), eps=1e-14, max_iter=10_000)
-    assert not res.converged
-    h = np.array(res.history)
-    assert res.iterations < 10_000
-    # the last 20 iterations set no new minimum of r^T r
-    assert h[-20:].min() >= h[:-20].min()
+    res = O.solve_cg(lambda v: A @ v + 0.5 * z, np.ones(30), eps=1e-14, max_iter=500)
+    assert not res.converged and res.iterations == 500 and len(res.history) == 500
 
 
 def test_cg_matches_textbook_on_diagonal():
