@@ -1,0 +1,198 @@
+"""Benchmark of the LS-SVM training hot path on one MI355X.
+
+One step = one full training (layout, q-vector, right-hand side, CG with one
+implicit Q~ product per iteration, bias) plus the prediction of 1024 held-out
+points, on synthetic data already resident in HBM. Default workload: cubic
+polynomial kernel, fp32, n = 32768 points x d = 4096 features, C = 1,
+eps = 1e-5.
+
+Prints one JSON line. `value` is the whole-step throughput in GFLOP/s with
+the symmetric count N(N+1)d per implicit product (N = n - 1) plus
+2 n_test n d for the prediction. `roofline` is the tile kernel's own rate:
+N(N+1)d divided by its average duration, measured with HIP events recorded
+on the launch stream over the timed steps. `cpu_baseline` times the CPU
+oracle's explicit row-panel product on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "implicit kernel matvec GFLOP/s (% MFMA peak); CG time-to-eps per training"
+PEAK_TFLOPS = {"f32": 157.3, "f64": 78.6}      # MI355X dense matrix-core peaks
+HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "lssvm_internal.h"):
+        with open(os.path.join(ROOT, "paper_2202_12674_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_record(workload: str):
+    """HBM bytes per tile-kernel launch from committed rocprofv3 counter runs,
+    or None when missing or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"k_tiles_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(cfg, X, budget_s: float):
+    """The oracle's explicit row-panel product Q~[rows] @ p on the host cores."""
+    import numpy as np
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()
+                       if t.get("user_api") == "blas"] or [1])
+    except Exception:  # noqa: BLE001
+        threads = len(os.sched_getaffinity(0))
+    spec = O.KernelSpec(cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+    N = cfg.n - 1
+    p = np.random.default_rng(12345).standard_normal(N)
+    X64 = X.astype(np.float64)
+    panel = 256
+    rows_done = 0
+    t0 = time.perf_counter()
+    start = 0
+    while True:
+        rows = np.arange(start, min(N, start + panel))
+        _ = O.reduced_rows(X64, spec, cfg.C, rows) @ p
+        rows_done += len(rows)
+        start = (start + panel) % N
+        if time.perf_counter() - t0 >= budget_s or rows_done >= N:
+            break
+    dt = time.perf_counter() - t0
+    flops = rows_done * (N + 1) * cfg.d          # share of the symmetric count N(N+1)d
+    return {"value": flops / dt / 1e9, "unit": "GFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{rows_done} of {N} rows of the explicit reduced matrix (fp64, "
+                      f"panels of {panel}) times a vector, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="poly_f32_32768x4096")
+    ap.add_argument("--n-test", type=int, default=1024)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2202_12674_amd as P
+    import synthdata as S
+
+    cfg = S.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    log(f"[bench] generating {cfg.name}")
+    X, y, scale = S.make_train(cfg)
+    Xte, _ = S.make_test(cfg, scale, n_test=args.n_test)
+    Xd = torch.from_numpy(X).to(dev)
+    yd = torch.from_numpy(y).to(dev)
+    Xted = torch.from_numpy(Xte).to(dev)
+    kw = dict(kernel=cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+    ws = P.alloc_workspace(P.workspace_bytes(cfg.n, cfg.d, Xd.dtype), dev)
+    wsp = P.alloc_workspace(P.predict_workspace_bytes(cfg.n, args.n_test, cfg.d, Xd.dtype), dev)
+    torch.cuda.synchronize()
+
+    def step():
+        r = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, max_iter=cfg.max_iter, workspace=ws,
+                    time_matvec=True, **kw)
+        P.predict(Xd, r.alpha, r.b, Xted, workspace=wsp, **kw)
+        return r
+
+    for i in range(args.warmup):
+        r = step()
+        log(f"[bench] warmup {i}: {r.iterations} it, train {r.t_total_ms:.1f} ms")
+    torch.cuda.synchronize()
+    results, walls = [], []
+    t_all = time.perf_counter()
+    for i in range(args.steps):
+        t0 = time.perf_counter()
+        r = step()
+        torch.cuda.synchronize()
+        walls.append((time.perf_counter() - t0) * 1e3)
+        results.append(r)
+        log(f"[bench] step {i}: {r.iterations} it, train {r.t_total_ms:.1f} ms, "
+            f"matvec avg {r.t_matvec_ms / max(1, r.n_matvec_timed):.3f} ms, "
+            f"wall {walls[-1]:.1f} ms")
+    torch.cuda.synchronize()
+    total_ms = (time.perf_counter() - t_all) * 1e3
+
+    N = cfg.n - 1
+    mv_flops = N * (N + 1) * cfg.d
+    pred_flops = 2 * args.n_test * cfg.n * cfg.d
+    n_mv = sum(r.n_matvec for r in results)
+    step_flops = (n_mv * mv_flops + len(results) * pred_flops)
+    ms_per_step = total_ms / args.steps
+    value = step_flops / (total_ms * 1e-3) / 1e9
+    mv_ms = sum(r.t_matvec_ms for r in results) / max(1, sum(r.n_matvec_timed for r in results))
+    achieved = mv_flops / (mv_ms * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    traffic = traffic_record(cfg.name)
+    train_ms = [r.t_total_ms for r in results]
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n": cfg.n, "d": cfg.d, "kernel": cfg.kernel,
+                   "gamma": cfg.gamma, "coef0": cfg.coef0, "degree": cfg.degree, "C": cfg.C,
+                   "eps": cfg.eps, "n_test": args.n_test},
+        "time_to_eps_ms": round(statistics.median(train_ms), 3),
+        "time_to_eps_cov": round(statistics.pstdev(train_ms) / statistics.mean(train_ms), 4),
+        "cg_iterations": results[-1].iterations,
+        "n_matvec_per_step": results[-1].n_matvec,
+        "matvec_ms": round(mv_ms, 4),
+        "matvec_gflops": round(mv_flops / (mv_ms * 1e-3) / 1e9, 2),
+        "matvec_dense_equiv_gflops": round(2 * N * N * cfg.d / (mv_ms * 1e-3) / 1e9, 2),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": traffic},
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample")
+        line["cpu_baseline"] = cpu_baseline(cfg, X, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

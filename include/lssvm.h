@@ -1,0 +1,166 @@
+/*
+ * lssvm.h - C ABI of the MI355X (gfx950) LS-SVM training hot path.
+ *
+ * Least-squares SVM training as in PLSSVM (arXiv 2202.12674): the bordered
+ * system of Sec. II-F, Eq. (11), [Q 1; 1^T 0][alpha; b] = [y; 0] with
+ * Q_ij = k(x_i, x_j) + delta_ij / C, is reduced around the last point
+ * m = n - 1 (Eqs. (12)-(14)) to the SPD system
+ *     Q~ alpha~ = ybar - y_m 1,      N = n - 1 unknowns,
+ * which is solved by conjugate gradients (Sec. III-B). Q~ is never stored:
+ * every product Q~ p recomputes its entries (Eq. (16))
+ *     Q~_ij = k(x_i,x_j) + delta_ij/C - k(x_m,x_j) - k(x_i,x_m) + k(x_m,x_m) + 1/C
+ * tile by tile on the matrix cores. alpha_m = -sum(alpha~) (last row of
+ * Eq. (11)) and b follows Eq. (15).
+ *
+ * Conventions shared by every entry point:
+ * - Array arguments are DEVICE pointers unless marked "host". The caller
+ *   owns all memory; the library allocates no device memory. Scratch space
+ *   comes from the caller's `workspace` (device, 256-byte aligned, at least
+ *   the size reported by the matching *_workspace_bytes call).
+ * - dtype is LSSVM_F64 or LSSVM_F32 and applies to every floating-point
+ *   device array of the call. In LSSVM_F32 the point data, the matrix-core
+ *   contraction and the kernel epilogue are fp32; CG vectors, dot products,
+ *   CG scalars and b are fp64.
+ * - Points are n x d, row-major (point i's d features contiguous).
+ * - All work is enqueued on `stream` (a hipStream_t; NULL = default stream)
+ *   and the call returns only after it has finished.
+ * - Return value: LSSVM_OK (0), LSSVM_NOT_CONVERGED (1, outputs hold the last
+ *   iterate) or a negative error code; on error the outputs are unspecified
+ *   and lssvm_last_error() describes the cause. Argument checks run on the
+ *   host before any GPU work. No C++ exception crosses this boundary.
+ * - Calls on one stream are serialised by the caller; calls that share a
+ *   workspace must not overlap.
+ */
+#ifndef LSSVM_H_
+#define LSSVM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of every floating-point device array of a call. */
+enum { LSSVM_F64 = 0, LSSVM_F32 = 1 };
+
+/* Kernel functions of Sec. II-E (kernel table). */
+enum {
+    LSSVM_LINEAR = 0, /* <x, z>                                  */
+    LSSVM_POLY = 1,   /* (gamma <x, z> + coef0)^degree, gamma > 0 */
+    LSSVM_RBF = 2     /* exp(-gamma ||x - z||^2),       gamma > 0 */
+};
+
+/* Status codes. */
+enum {
+    LSSVM_OK = 0,
+    LSSVM_NOT_CONVERGED = 1, /* max_iter reached before eps; outputs = last iterate    */
+    LSSVM_EINVAL = -1,       /* bad argument (checked on the host, no GPU work done)  */
+    LSSVM_ENONFINITE = -2,   /* X (or X_test) holds a NaN or an infinity              */
+    LSSVM_EBADLABEL = -3,    /* a label is not exactly +1 or -1                       */
+    LSSVM_EBREAKDOWN = -4,   /* CG curvature d^T Q~ d <= 0 or not finite              */
+    LSSVM_EHIP = -5          /* a HIP runtime call failed                             */
+};
+
+/* Kernel parameters (Sec. II-E). gamma: poly and rbf (> 0). coef0: the
+ * polynomial's additive constant r (>= 0 keeps Q~ positive definite).
+ * degree: the polynomial's exponent (>= 1). Ignored where unused. */
+typedef struct lssvm_params {
+    double gamma;
+    double coef0;
+    int32_t degree;
+} lssvm_params;
+
+/* Training report (host struct). Fields marked "in" are read by the library,
+ * all others are written by it. */
+typedef struct lssvm_info {
+    int64_t iterations;            /* CG iterations performed                        */
+    int64_t n_matvec;              /* implicit Q~ products (incl. residual refreshes) */
+    double rel_residual;           /* sqrt(r^T r / r0^T r0) of the CG recurrence      */
+    double true_rel_residual;      /* ||rhs - Q~ x|| / ||rhs|| if requested, else -1  */
+    double t_setup_ms;             /* layout, q-vector, right-hand side               */
+    double t_cg_ms;                /* CG loop                                         */
+    double t_total_ms;             /* whole call                                      */
+    int32_t compute_true_residual; /* in: nonzero -> one extra product at the end     */
+    int32_t reserved;
+    double* residual_history;      /* in: host array or NULL; receives r^T r / r0^T r0
+                                      after each iteration                           */
+    int64_t history_capacity;      /* in: length of residual_history                 */
+    int32_t time_matvec;           /* in: nonzero -> time every Q~ product with HIP
+                                      events recorded on `stream`                    */
+    int32_t reserved2;
+    double t_matvec_ms;            /* sum of the timed Q~ products (tile kernel only) */
+    int64_t n_matvec_timed;        /* number of products in t_matvec_ms              */
+} lssvm_info;
+
+/* Device workspace needed by lssvm_train and lssvm_matvec for n points of
+ * d features. Returns 0 if n < 1, d < 1 or dtype is unknown. */
+size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype);
+
+/* Device workspace needed by lssvm_predict. Returns 0 on bad sizes/dtype. */
+size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32_t dtype);
+
+/*
+ * Train an LS-SVM (Sec. II-F, Eqs. (11)-(15); CG of Sec. III-B).
+ *
+ * X         device, n x d row-major, dtype. Must be finite.
+ * y         device, n labels, dtype, each exactly +1 or -1.
+ * n, d      n >= 1 points, d >= 1 features.
+ * kernel    LSSVM_LINEAR / LSSVM_POLY / LSSVM_RBF; kp its parameters (host, may
+ *           be NULL for LSSVM_LINEAR).
+ * C         regularisation, finite and > 0.
+ * eps       relative-residual target, 0 < eps < 1: CG stops once
+ *           r^T r <= eps^2 r0^T r0 (x0 = 0, r0 = ybar - y_m 1).
+ * max_iter  iteration cap; 0 means N = n - 1.
+ * alpha_out device, n values, dtype: alpha~ followed by alpha_m = -sum(alpha~).
+ * b_out     host, the bias of Eq. (15).
+ * info      host, may be NULL.
+ * CG details: the residual is recomputed as rhs - Q~ x every 50th iteration;
+ * reaching max_iter without meeting eps returns LSSVM_NOT_CONVERGED. n = 1
+ * or all labels equal give alpha = 0, b = y_m without iterating.
+ */
+int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtype,
+                int32_t kernel, const lssvm_params* kp, double C, double eps,
+                int64_t max_iter, void* workspace, size_t workspace_bytes,
+                void* alpha_out, double* b_out, lssvm_info* info, void* stream);
+
+/*
+ * Score points with a trained model: f(x) = sum_i alpha_i k(x_i, x) + b
+ * (Eq. (10) with the sign carried by alpha), label +1 iff f(x) > 0 else -1.
+ *
+ * X_train    device, n x d row-major, dtype; alpha device, n values, dtype.
+ * X_test     device, n_test x d row-major, dtype, n_test >= 1. Must be finite.
+ * scores_out device, n_test values, dtype.
+ * labels_out device, n_test int32 values (+1/-1), may be NULL.
+ */
+int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, int64_t d,
+                  int32_t dtype, int32_t kernel, const lssvm_params* kp,
+                  const void* X_test, int64_t n_test, void* workspace,
+                  size_t workspace_bytes, void* scores_out, int32_t* labels_out,
+                  void* stream);
+
+/*
+ * One implicit product out = Q~ p of the reduced system (Eqs. (13), (16)),
+ * the unit of work of each CG iteration.
+ *
+ * X     device, n x d row-major, dtype, n >= 2.
+ * p     device, N = n - 1 values, dtype. out device, N values, dtype.
+ * Uses the lssvm_workspace_bytes(n, d, dtype) workspace.
+ */
+int lssvm_matvec(const void* X, int64_t n, int64_t d, int32_t dtype, int32_t kernel,
+                 const lssvm_params* kp, double C, const void* p, void* out,
+                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Message for the last failing call on this thread ("" if none). The pointer
+ * stays valid until the next call on this thread. */
+const char* lssvm_last_error(void);
+
+/* Tile edge (points per tile) that the matrix-core kernels use for dtype,
+ * 0 for an unknown dtype. Informational: sizes need no padding by the caller. */
+int32_t lssvm_tile_size(int32_t dtype);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSSVM_H_ */

@@ -1,0 +1,14 @@
+"""MI355X-native LS-SVM training hot path (PLSSVM, arXiv 2202.12674).
+
+The reduced LS-SVM system of Sec. II-F is solved by conjugate gradients
+(Sec. III-B) with the implicit reduced-matrix product of Eq. (16) on the
+gfx950 matrix cores. The public entry points wrap the C ABI of
+include/lssvm.h; PyTorch supplies device memory and streams only.
+"""
+from ._binding import (F32, F64, LINEAR, POLY, RBF, LssvmError, TrainResult,  # noqa: F401
+                       alloc_workspace, last_error, lib, matvec, predict,
+                       predict_workspace_bytes, train, workspace_bytes)
+from .build import LIB_PATH, build  # noqa: F401
+
+__all__ = ["train", "predict", "matvec", "workspace_bytes", "predict_workspace_bytes",
+           "alloc_workspace", "LssvmError", "TrainResult", "lib", "last_error", "build"]

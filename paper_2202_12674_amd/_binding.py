@@ -1,0 +1,244 @@
+"""ctypes binding of liblssvm.so (C ABI in include/lssvm.h).
+
+Argument marshalling only: every step of the path runs in the HIP library.
+PyTorch provides device memory and the current stream. There is no CPU
+fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblssvm.so")
+
+F64, F32 = 0, 1
+LINEAR, POLY, RBF = 0, 1, 2
+OK, NOT_CONVERGED, EINVAL, ENONFINITE, EBADLABEL, EBREAKDOWN, EHIP = 0, 1, -1, -2, -3, -4, -5
+KERNELS = {"linear": LINEAR, "poly": POLY, "polynomial": POLY, "rbf": RBF}
+STATUS_NAMES = {OK: "OK", NOT_CONVERGED: "NOT_CONVERGED", EINVAL: "EINVAL",
+                ENONFINITE: "ENONFINITE", EBADLABEL: "EBADLABEL", EBREAKDOWN: "EBREAKDOWN",
+                EHIP: "EHIP"}
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_double), ("coef0", ctypes.c_double),
+                ("degree", ctypes.c_int32)]
+
+
+class Info(ctypes.Structure):
+    _fields_ = [("iterations", ctypes.c_int64), ("n_matvec", ctypes.c_int64),
+                ("rel_residual", ctypes.c_double), ("true_rel_residual", ctypes.c_double),
+                ("t_setup_ms", ctypes.c_double), ("t_cg_ms", ctypes.c_double),
+                ("t_total_ms", ctypes.c_double), ("compute_true_residual", ctypes.c_int32),
+                ("reserved", ctypes.c_int32),
+                ("residual_history", ctypes.POINTER(ctypes.c_double)),
+                ("history_capacity", ctypes.c_int64), ("time_matvec", ctypes.c_int32),
+                ("reserved2", ctypes.c_int32), ("t_matvec_ms", ctypes.c_double),
+                ("n_matvec_timed", ctypes.c_int64)]
+
+
+class LssvmError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+_SIGS = {
+    "lssvm_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32]),
+    "lssvm_predict_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64,
+                                                        ctypes.c_int64, ctypes.c_int32]),
+    "lssvm_train": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                   ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.POINTER(Params), ctypes.c_double, ctypes.c_double,
+                                   ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(Info), ctypes.c_void_p]),
+    "lssvm_predict": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_double,
+                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.POINTER(Params), ctypes.c_void_p,
+                                     ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "lssvm_matvec": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(Params),
+                                    ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "lssvm_last_error": (ctypes.c_char_p, []),
+    "lssvm_tile_size": (ctypes.c_int32, [ctypes.c_int32]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2202_12674_amd.build` (no CPU fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().lssvm_last_error().decode()
+
+
+def _check(code: int, allow_not_converged: bool = False) -> int:
+    if code < 0 or (code == NOT_CONVERGED and not allow_not_converged):
+        raise LssvmError(code, last_error())
+    return code
+
+
+# ------------------------------------------------------------ torch layer ---
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float64:
+        return F64
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}; use float64 or float32")
+
+
+def _dev_ptr(t, name: str):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _params(kernel: str, gamma: float, coef0: float, degree: int):
+    if kernel not in KERNELS:
+        raise ValueError(f"unknown kernel {kernel!r}")
+    return KERNELS[kernel], Params(float(gamma), float(coef0), int(degree))
+
+
+def workspace_bytes(n: int, d: int, dtype) -> int:
+    torch = _torch()
+    code = F64 if dtype == torch.float64 else F32
+    return int(lib().lssvm_workspace_bytes(n, d, code))
+
+
+def predict_workspace_bytes(n: int, n_test: int, d: int, dtype) -> int:
+    torch = _torch()
+    code = F64 if dtype == torch.float64 else F32
+    return int(lib().lssvm_predict_workspace_bytes(n, n_test, d, code))
+
+
+def alloc_workspace(nbytes: int, device):
+    torch = _torch()
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+@dataclasses.dataclass
+class TrainResult:
+    alpha: object            # torch tensor (n,), dtype of X
+    b: float
+    status: int
+    converged: bool
+    iterations: int
+    n_matvec: int
+    rel_residual: float
+    true_rel_residual: float
+    t_setup_ms: float
+    t_cg_ms: float
+    t_total_ms: float
+    history: list
+    t_matvec_ms: float = 0.0
+    n_matvec_timed: int = 0
+
+
+def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
+          degree: int = 1, C: float = 1.0, eps: float = 1e-8, max_iter: int = 0,
+          workspace=None, true_residual: bool = False, history: int = 0,
+          raise_not_converged: bool = False, time_matvec: bool = False) -> TrainResult:
+    """lssvm_train on device tensors X (n x d) and y (n,), same float dtype."""
+    torch = _torch()
+    n, d = X.shape
+    dt = _dtype_code(X)
+    if y.dtype != X.dtype or y.shape != (n,):
+        raise ValueError("y must have shape (n,) and the dtype of X")
+    k, kp = _params(kernel, gamma, coef0, degree)
+    if workspace is None:
+        workspace = alloc_workspace(lib().lssvm_workspace_bytes(n, d, dt), X.device)
+    alpha = torch.empty(n, dtype=X.dtype, device=X.device)
+    b = ctypes.c_double(0.0)
+    info = Info()
+    info.compute_true_residual = 1 if true_residual else 0
+    info.time_matvec = 1 if time_matvec else 0
+    hist = (ctypes.c_double * history)() if history > 0 else None
+    if hist is not None:
+        info.residual_history = ctypes.cast(hist, ctypes.POINTER(ctypes.c_double))
+        info.history_capacity = history
+    code = lib().lssvm_train(_dev_ptr(X, "X"), _dev_ptr(y, "y"), n, d, dt, k, ctypes.byref(kp),
+                             float(C), float(eps), int(max_iter), _dev_ptr(workspace, "workspace"),
+                             workspace.numel(), _dev_ptr(alpha, "alpha"), ctypes.byref(b),
+                             ctypes.byref(info), _stream(X.device))
+    _check(code, allow_not_converged=not raise_not_converged)
+    return TrainResult(alpha, b.value, code, code == OK, info.iterations, info.n_matvec,
+                       info.rel_residual, info.true_rel_residual, info.t_setup_ms, info.t_cg_ms,
+                       info.t_total_ms,
+                       list(hist[:min(history, info.iterations)]) if hist is not None else [],
+                       info.t_matvec_ms, info.n_matvec_timed)
+
+
+def predict(X_train, alpha, b: float, X_test, kernel: str = "linear", gamma: float = 1.0,
+            coef0: float = 0.0, degree: int = 1, workspace=None, want_labels: bool = True):
+    """lssvm_predict: (scores, labels) for the rows of X_test."""
+    torch = _torch()
+    n, d = X_train.shape
+    nt = X_test.shape[0]
+    dt = _dtype_code(X_train)
+    k, kp = _params(kernel, gamma, coef0, degree)
+    if workspace is None:
+        workspace = alloc_workspace(lib().lssvm_predict_workspace_bytes(n, nt, d, dt),
+                                    X_train.device)
+    scores = torch.empty(nt, dtype=X_train.dtype, device=X_train.device)
+    labels = torch.empty(nt, dtype=torch.int32, device=X_train.device) if want_labels else None
+    code = lib().lssvm_predict(_dev_ptr(X_train, "X_train"), _dev_ptr(alpha, "alpha"), float(b),
+                               n, d, dt, k, ctypes.byref(kp), _dev_ptr(X_test, "X_test"), nt,
+                               _dev_ptr(workspace, "workspace"), workspace.numel(),
+                               _dev_ptr(scores, "scores"),
+                               _dev_ptr(labels, "labels") if labels is not None else None,
+                               _stream(X_train.device))
+    _check(code)
+    return scores, labels
+
+
+def matvec(X, p, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
+           degree: int = 1, C: float = 1.0, workspace=None, out=None):
+    """lssvm_matvec: out = Q~ p for the reduced system of the points X."""
+    torch = _torch()
+    n, d = X.shape
+    dt = _dtype_code(X)
+    k, kp = _params(kernel, gamma, coef0, degree)
+    if workspace is None:
+        workspace = alloc_workspace(lib().lssvm_workspace_bytes(n, d, dt), X.device)
+    if out is None:
+        out = torch.empty(n - 1, dtype=X.dtype, device=X.device)
+    code = lib().lssvm_matvec(_dev_ptr(X, "X"), n, d, dt, k, ctypes.byref(kp), float(C),
+                              _dev_ptr(p, "p"), _dev_ptr(out, "out"),
+                              _dev_ptr(workspace, "workspace"), workspace.numel(),
+                              _stream(X.device))
+    _check(code)
+    return out

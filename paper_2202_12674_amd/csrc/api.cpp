@@ -1,0 +1,649 @@
+// Host runtime of the C ABI declared in include/lssvm.h: argument checks,
+// workspace carve-up, the CG driver loop (Sec. III-B) and the bias step
+// (Eq. (15)). Every numeric step runs in the gfx950 kernels of kernels.hip;
+// this file only validates, sequences launches and reads back scalars.
+#include "lssvm.h"
+#include "lssvm_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+namespace lssvm {
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+#define LSSVM_HIP(call)                                                                  \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(LSSVM_EHIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_),     \
+                  __FILE__, __LINE__);                                                   \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kReplaceEvery = 50;  // residual recomputed every 50th iteration
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+using clock_t_ = std::chrono::steady_clock;
+inline double ms_since(clock_t_::time_point t0) {
+  return std::chrono::duration<double, std::milli>(clock_t_::now() - t0).count();
+}
+
+// Padded sizes for n points of d features (element type T).
+struct Geometry {
+  int64_t n, d, N;  // N = n - 1 unknowns of the reduced system
+  int64_t tile, bk;
+  int64_t ld;       // points per feature row of the layout (>= n, multiple of tile)
+  int64_t d_pad;    // features, multiple of bk
+  int64_t nT;       // tiles per edge of the reduced system
+  int64_t NP;       // nT * tile: padded length of every CG vector
+  int64_t nb;       // blocks of 256 over NP
+};
+
+template <typename T>
+Geometry geometry(int64_t n, int64_t d) {
+  Geometry g{};
+  g.n = n;
+  g.d = d;
+  g.N = n - 1;
+  g.tile = TileShape<T>::T;
+  g.bk = TileShape<T>::BK;
+  g.ld = round_up(n, g.tile);
+  g.d_pad = round_up(d, g.bk);
+  g.nT = (g.N + g.tile - 1) / g.tile;
+  g.NP = g.nT * g.tile;
+  g.nb = (g.NP + 255) / 256;
+  return g;
+}
+
+// Carves aligned sub-buffers out of the caller's workspace (or only sizes them).
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <typename U>
+  U* take(int64_t count) {
+    U* p = base ? reinterpret_cast<U*>(base + off) : nullptr;
+    off = align_up(off + (size_t)count * sizeof(U));
+    return p;
+  }
+};
+
+template <typename T>
+struct TrainWs {
+  T* Xt;
+  T* norms;
+  T* qT;
+  double* q64;
+  double* part;
+  double *rhs, *x, *r, *dir, *qv;
+  T* pT;
+  double *bp0, *bp1;
+  double* scal;
+  int* flags;
+  size_t bytes;
+};
+
+template <typename T>
+TrainWs<T> carve_train(const Geometry& g, void* base) {
+  Carver c(base);
+  TrainWs<T> w{};
+  w.Xt = c.take<T>(g.d_pad * g.ld);
+  w.norms = c.take<T>(g.ld);
+  w.qT = c.take<T>(g.ld);
+  w.q64 = c.take<double>(g.ld);
+  w.part = c.take<double>(g.nT * g.NP);
+  w.rhs = c.take<double>(g.NP);
+  w.x = c.take<double>(g.NP);
+  w.r = c.take<double>(g.NP);
+  w.dir = c.take<double>(g.NP);
+  w.qv = c.take<double>(g.NP);
+  w.pT = c.take<T>(g.NP);
+  w.bp0 = c.take<double>(g.nb + 1);
+  w.bp1 = c.take<double>(g.nb + 1);
+  w.scal = c.take<double>(S_COUNT);
+  w.flags = c.take<int>(F_COUNT);
+  w.bytes = c.off;
+  return w;
+}
+
+template <typename T>
+struct PredictWs {
+  T *Xtr, *ntr, *alpha;
+  T *Xte, *nte;
+  double* part;
+  int* flags;
+  int64_t ld_te, nTc, nTr;
+  size_t bytes;
+};
+
+template <typename T>
+PredictWs<T> carve_predict(const Geometry& g, int64_t n_test, void* base) {
+  Carver c(base);
+  PredictWs<T> w{};
+  w.ld_te = round_up(n_test, g.tile);
+  w.nTc = g.ld / g.tile;
+  w.nTr = w.ld_te / g.tile;
+  w.Xtr = c.take<T>(g.d_pad * g.ld);
+  w.ntr = c.take<T>(g.ld);
+  w.alpha = c.take<T>(g.ld);
+  w.Xte = c.take<T>(g.d_pad * w.ld_te);
+  w.nte = c.take<T>(w.ld_te);
+  w.part = c.take<double>(w.nTc * w.ld_te);
+  w.flags = c.take<int>(F_COUNT);
+  w.bytes = c.off;
+  return w;
+}
+
+// Pinned host buffer for the few scalars read back per iteration.
+struct HostScratch {
+  double* p = nullptr;
+  int* flags = nullptr;
+  hipError_t ensure() {
+    if (p) return hipSuccess;
+    void* v = nullptr;
+    hipError_t e = hipHostMalloc(&v, 64 * sizeof(double), hipHostMallocDefault);
+    if (e != hipSuccess) return e;
+    p = static_cast<double*>(v);
+    flags = reinterpret_cast<int*>(p + 32);
+    return hipSuccess;
+  }
+};
+thread_local HostScratch g_host;
+
+// HIP events around each implicit product, recorded on the launch stream.
+struct MatvecTimer {
+  bool on = false;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  int used = 0;          // event pairs recorded since the last harvest
+  double total_ms = 0.0;
+  int64_t count = 0;
+  hipError_t init(bool enable) {
+    on = enable;
+    if (!on) return hipSuccess;
+    for (auto& e : ev) {
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  ~MatvecTimer() {
+    for (auto& e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+  hipError_t start(hipStream_t s) { return on ? hipEventRecord(ev[2 * used], s) : hipSuccess; }
+  hipError_t stop(hipStream_t s) {
+    if (!on) return hipSuccess;
+    hipError_t r = hipEventRecord(ev[2 * used + 1], s);
+    ++used;
+    return r;
+  }
+  // After the stream has been synchronised: add the recorded pairs.
+  hipError_t harvest() {
+    for (int i = 0; i < used; ++i) {
+      float ms = 0.f;
+      hipError_t r = hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]);
+      if (r != hipSuccess) return r;
+      total_ms += ms;
+      ++count;
+    }
+    used = 0;
+    return hipSuccess;
+  }
+};
+
+bool valid_dtype(int32_t dt) { return dt == LSSVM_F64 || dt == LSSVM_F32; }
+bool valid_kernel(int32_t k) { return k == LSSVM_LINEAR || k == LSSVM_POLY || k == LSSVM_RBF; }
+
+int check_kernel_params(int32_t kernel, const lssvm_params* kp) {
+  if (!valid_kernel(kernel)) return fail(LSSVM_EINVAL, "unknown kernel %d", (int)kernel);
+  if (kernel == LSSVM_LINEAR) return LSSVM_OK;
+  if (!kp) return fail(LSSVM_EINVAL, "kernel parameters required for kernel %d", (int)kernel);
+  if (!(kp->gamma > 0.0) || !std::isfinite(kp->gamma))
+    return fail(LSSVM_EINVAL, "gamma must be finite and > 0 (got %g)", kp->gamma);
+  if (kernel == LSSVM_POLY) {
+    if (kp->degree < 1) return fail(LSSVM_EINVAL, "degree must be >= 1 (got %d)", kp->degree);
+    if (!std::isfinite(kp->coef0)) return fail(LSSVM_EINVAL, "coef0 must be finite");
+  }
+  return LSSVM_OK;
+}
+
+int check_sizes(int64_t n, int64_t d, int64_t min_n) {
+  if (n < min_n) return fail(LSSVM_EINVAL, "n must be >= %lld (got %lld)", (long long)min_n,
+                             (long long)n);
+  if (d < 1) return fail(LSSVM_EINVAL, "d must be >= 1 (got %lld)", (long long)d);
+  // the layout grid has ceil(d / 64) blocks in y (<= 65535) and the
+  // triangle of tiles must fit one 32-bit grid dimension
+  if (n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
+    return fail(LSSVM_EINVAL, "problem too large (n=%lld, d=%lld)", (long long)n, (long long)d);
+  return LSSVM_OK;
+}
+
+int check_workspace(const void* ws, size_t have, size_t need) {
+  if (!ws) return fail(LSSVM_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+    return fail(LSSVM_EINVAL, "workspace must be %zu-byte aligned", kAlign);
+  if (have < need)
+    return fail(LSSVM_EINVAL, "workspace too small: %zu bytes given, %zu needed", have, need);
+  return LSSVM_OK;
+}
+
+template <typename T>
+TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
+                     double C, const T* p) {
+  TileArgs<T> a{};
+  a.A = w.Xt;
+  a.B = w.Xt;
+  a.lda = g.ld;
+  a.ldb = g.ld;
+  a.nkb = g.d_pad / g.bk;
+  a.nA = w.norms;
+  a.nB = w.norms;
+  a.qA = w.qT;
+  a.qB = w.qT;
+  a.pA = p;
+  a.pB = p;
+  a.gamma = (T)kp.gamma;
+  a.coef0 = (T)kp.coef0;
+  a.degree = kp.degree;
+  a.qmm = (T)(kmm + 1.0 / C);
+  a.invC = (T)(1.0 / C);
+  a.nTc = g.nT;
+  a.part = w.part;
+  a.part_ld = g.NP;
+  return a;
+}
+
+inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
+
+// a1 + a2: layout, norms, q and k_mm; reads back k_mm and the input flags.
+template <typename T>
+int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
+                 const lssvm_params& kp, hipStream_t s, double* kmm) {
+  LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
+  LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
+  LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d, g.N, g.N, kernel, kp.gamma, kp.coef0, kp.degree,
+                              w.norms, w.qT, w.q64, w.scal, s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+                           s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_KMM, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+  *kmm = g_host.p[0];
+  return LSSVM_OK;
+}
+
+// One implicit product Q~ p into the partial-sum buffer.
+template <typename T>
+int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
+                    double C, int32_t kernel, const T* p, hipStream_t s) {
+  TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
+  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT), s));
+  return LSSVM_OK;
+}
+
+template <typename T>
+int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
+                 double C, int32_t kernel, const T* p, hipStream_t s, MatvecTimer& tm) {
+  LSSVM_HIP(tm.start(s));
+  TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
+  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, g.nT * (g.nT + 1) / 2, s));
+  LSSVM_HIP(tm.stop(s));
+  return LSSVM_OK;
+}
+
+#define LSSVM_TRY(expr)      \
+  do {                       \
+    int rc_ = (expr);        \
+    if (rc_ != LSSVM_OK) return rc_; \
+  } while (0)
+
+template <typename T>
+int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
+               const lssvm_params& kp, double C, double eps, int64_t max_iter, void* workspace,
+               size_t ws_bytes, T* alpha_out, double* b_out, lssvm_info* info, hipStream_t s) {
+  const auto t0 = clock_t_::now();
+  const Geometry g = geometry<T>(n, d);
+  TrainWs<T> w = carve_train<T>(g, nullptr);
+  LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
+  w = carve_train<T>(g, workspace);
+  LSSVM_HIP(g_host.ensure());
+
+  if (info) {
+    info->iterations = 0;
+    info->n_matvec = 0;
+    info->t_matvec_ms = 0.0;
+    info->n_matvec_timed = 0;
+    info->rel_residual = 0.0;
+    info->true_rel_residual = -1.0;
+    info->t_setup_ms = info->t_cg_ms = info->t_total_ms = 0.0;
+  }
+
+  if (n == 1) {  // alpha = [0], b = y_0
+    LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
+    LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
+    LSSVM_HIP(launch_single_point<T>(y, alpha_out, w.scal, w.flags, s));
+    LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int),
+                             hipMemcpyDeviceToHost, s));
+    LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
+    LSSVM_HIP(hipStreamSynchronize(s));
+    if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+    if (g_host.flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
+    *b_out = g_host.p[0];
+    if (info) {
+      info->rel_residual = 0.0;
+      info->true_rel_residual = info->compute_true_residual ? 0.0 : -1.0;
+      info->t_total_ms = ms_since(t0);
+    }
+    return LSSVM_OK;
+  }
+
+  // ---- setup: a1, a2, a3
+  double kmm = 0.0;
+  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
+  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.pT, w.bp0, w.flags, s));
+  LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+                           s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  if (g_host.flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
+  const double delta0 = g_host.p[0];
+  const double t_setup = ms_since(t0);
+  MatvecTimer tm;
+  LSSVM_HIP(tm.init(info && info->time_matvec));
+
+  // ---- a4 + a5: conjugate gradients
+  const auto t1 = clock_t_::now();
+  if (max_iter <= 0) max_iter = g.N;
+  int64_t it = 0, nmv = 0;
+  bool converged = delta0 == 0.0;  // all labels equal: alpha~ = 0 solves the system
+  double delta = delta0;
+  int status = LSSVM_OK;
+  const double stop = eps * eps * delta0;
+  while (!converged && it < max_iter) {
+    ++it;
+    const int par = (int)((it - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
+    LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.pT, s, tm));
+    ++nmv;
+    LSSVM_HIP(launch_cg_gather(w.part, g.nT, g.NP, g.N, w.dir, w.qv, w.bp0, s));
+    if (it % kReplaceEvery == 0) {
+      LSSVM_HIP(launch_cg_update<T>(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.pT,
+                                    w.bp1, g.NP, s));
+      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.pT, s, tm));
+      ++nmv;
+      LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, s));
+    } else {
+      LSSVM_HIP(launch_cg_update<T>(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.pT,
+                                    w.bp1, g.NP, s));
+    }
+    LSSVM_HIP(launch_cg_direction<T>(w.bp1, g.nb, w.scal, par, it, w.r, w.dir, w.pT, g.NP, s));
+    LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_STATUS, 4 * sizeof(double),
+                             hipMemcpyDeviceToHost, s));
+    LSSVM_HIP(hipStreamSynchronize(s));
+    LSSVM_HIP(tm.harvest());
+    const double dnew = g_host.p[0], curv = g_host.p[1], step = g_host.p[2];
+    if (!(curv > 0.0) || !std::isfinite(curv) || !std::isfinite(step) || !std::isfinite(dnew)) {
+      status = fail(LSSVM_EBREAKDOWN, "CG breakdown at iteration %lld (d^T Q d = %g)",
+                    (long long)it, curv);
+      break;
+    }
+    delta = dnew;
+    if (info && info->residual_history && it <= info->history_capacity)
+      info->residual_history[it - 1] = delta / delta0;
+    if (delta <= stop) {
+      converged = true;
+      break;
+    }
+  }
+  const double t_cg = ms_since(t1);
+  if (status == LSSVM_OK && !converged) {
+    status = LSSVM_NOT_CONVERGED;
+    fail(LSSVM_NOT_CONVERGED, "CG stopped after %lld iterations at relative residual %g",
+         (long long)it, std::sqrt(delta / delta0));
+  }
+  if (status < 0) return status;
+
+  // ---- a6: alpha_m and b
+  LSSVM_HIP(launch_bias<T>(w.x, w.q64, g.N, y, w.scal, 1.0 / C, alpha_out, s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  *b_out = g_host.p[0];
+
+  if (info) {
+    info->iterations = it;
+    info->rel_residual = delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0;
+    if (info->compute_true_residual) {
+      double tr = 0.0;
+      if (delta0 > 0.0) {
+        LSSVM_HIP(launch_cast_vec<T>(w.x, w.pT, g.NP, s));
+        LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.pT, s));
+        LSSVM_HIP(launch_true_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.bp1, s));
+        LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
+        LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
+                                 hipMemcpyDeviceToHost, s));
+        LSSVM_HIP(hipStreamSynchronize(s));
+        tr = std::sqrt(g_host.p[0] / delta0);
+      }
+      info->true_rel_residual = tr;
+    }
+    info->n_matvec = nmv;
+    info->t_matvec_ms = tm.total_ms;
+    info->n_matvec_timed = tm.count;
+    info->t_setup_ms = t_setup;
+    info->t_cg_ms = t_cg;
+    info->t_total_ms = ms_since(t0);
+  }
+  return status;
+}
+
+template <typename T>
+int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_params& kp,
+                double C, const T* p, T* out, void* workspace, size_t ws_bytes, hipStream_t s) {
+  const Geometry g = geometry<T>(n, d);
+  TrainWs<T> w = carve_train<T>(g, nullptr);
+  LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
+  w = carve_train<T>(g, workspace);
+  LSSVM_HIP(g_host.ensure());
+  double kmm = 0.0;
+  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
+  LSSVM_HIP(launch_pad_vec<T>(p, g.N, w.pT, g.NP, s));
+  LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.pT, s));
+  LSSVM_HIP(launch_mv_out<T>(w.part, g.nT, g.NP, g.N, out, s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  return LSSVM_OK;
+}
+
+template <typename T>
+int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, int32_t kernel,
+                 const lssvm_params& kp, const T* Xte, int64_t n_test, void* workspace,
+                 size_t ws_bytes, T* scores, int32_t* labels, hipStream_t s) {
+  const Geometry g = geometry<T>(n, d);
+  PredictWs<T> w = carve_predict<T>(g, n_test, nullptr);
+  LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
+  w = carve_predict<T>(g, n_test, workspace);
+  LSSVM_HIP(g_host.ensure());
+  LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
+  LSSVM_HIP(launch_layout<T>(Xtr, n, d, w.Xtr, g.ld, g.d_pad, w.flags, s));
+  LSSVM_HIP(launch_layout<T>(Xte, n_test, d, w.Xte, w.ld_te, g.d_pad, w.flags, s));
+  if (kernel == LSSVM_RBF) {  // squared norms are only read by the radial kernel
+    LSSVM_HIP(launch_norms_q<T>(w.Xtr, g.ld, d, -1, 0, kernel, kp.gamma, kp.coef0, kp.degree,
+                                w.ntr, nullptr, nullptr, nullptr, s));
+    LSSVM_HIP(launch_norms_q<T>(w.Xte, w.ld_te, d, -1, 0, kernel, kp.gamma, kp.coef0,
+                                kp.degree, w.nte, nullptr, nullptr, nullptr, s));
+  }
+  LSSVM_HIP(launch_pad_vec<T>(alpha, n, w.alpha, g.ld, s));
+  TileArgs<T> a{};
+  a.A = w.Xte;
+  a.B = w.Xtr;
+  a.lda = w.ld_te;
+  a.ldb = g.ld;
+  a.nkb = g.d_pad / g.bk;
+  a.nA = w.nte;
+  a.nB = w.ntr;
+  a.qA = nullptr;
+  a.qB = nullptr;
+  a.pA = nullptr;
+  a.pB = w.alpha;
+  a.gamma = (T)kp.gamma;
+  a.coef0 = (T)kp.coef0;
+  a.degree = kp.degree;
+  a.nTc = w.nTc;
+  a.part = w.part;
+  a.part_ld = w.ld_te;
+  LSSVM_HIP(launch_tiles_gen<T>(a, kernel, w.nTr, s));
+  LSSVM_HIP(launch_predict_finish<T>(w.part, w.nTc, w.ld_te, n_test, b, scores, labels, s));
+  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+                           s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  if (g_host.flags[F_NONFINITE])
+    return fail(LSSVM_ENONFINITE, "X_train or X_test holds a NaN or an infinity");
+  return LSSVM_OK;
+}
+
+template <typename T>
+size_t train_bytes(int64_t n, int64_t d) {
+  return carve_train<T>(geometry<T>(n, d), nullptr).bytes;
+}
+
+template <typename T>
+size_t predict_bytes(int64_t n, int64_t n_test, int64_t d) {
+  return carve_predict<T>(geometry<T>(n, d), n_test, nullptr).bytes;
+}
+
+lssvm_params params_or_default(const lssvm_params* kp) {
+  lssvm_params p{1.0, 0.0, 1};
+  if (kp) p = *kp;
+  return p;
+}
+
+}  // namespace
+}  // namespace lssvm
+
+using namespace lssvm;
+
+extern "C" {
+
+size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype) {
+  if (n < 1 || d < 1 || !valid_dtype(dtype)) return 0;
+  return dtype == LSSVM_F64 ? train_bytes<double>(n, d) : train_bytes<float>(n, d);
+}
+
+size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32_t dtype) {
+  if (n < 1 || n_test < 1 || d < 1 || !valid_dtype(dtype)) return 0;
+  return dtype == LSSVM_F64 ? predict_bytes<double>(n, n_test, d)
+                            : predict_bytes<float>(n, n_test, d);
+}
+
+int32_t lssvm_tile_size(int32_t dtype) {
+  if (dtype == LSSVM_F64) return TileShape<double>::T;
+  if (dtype == LSSVM_F32) return TileShape<float>::T;
+  return 0;
+}
+
+const char* lssvm_last_error(void) { return g_last_error.c_str(); }
+
+int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtype,
+                int32_t kernel, const lssvm_params* kp, double C, double eps, int64_t max_iter,
+                void* workspace, size_t workspace_bytes, void* alpha_out, double* b_out,
+                lssvm_info* info, void* stream) {
+  try {
+    g_last_error.clear();
+    if (!X || !y || !alpha_out || !b_out) return fail(LSSVM_EINVAL, "NULL array argument");
+    if (!valid_dtype(dtype)) return fail(LSSVM_EINVAL, "unknown dtype %d", (int)dtype);
+    LSSVM_TRY(check_sizes(n, d, 1));
+    LSSVM_TRY(check_kernel_params(kernel, kp));
+    if (!(C > 0.0) || !std::isfinite(C)) return fail(LSSVM_EINVAL, "C must be finite and > 0");
+    if (!(eps > 0.0 && eps < 1.0)) return fail(LSSVM_EINVAL, "eps must lie in (0, 1)");
+    if (max_iter < 0) return fail(LSSVM_EINVAL, "max_iter must be >= 0");
+    if (info && info->residual_history == nullptr && info->history_capacity != 0)
+      return fail(LSSVM_EINVAL, "history_capacity without residual_history");
+    const lssvm_params p = params_or_default(kp);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == LSSVM_F64)
+      return train_impl<double>(static_cast<const double*>(X), static_cast<const double*>(y), n, d,
+                                kernel, p, C, eps, max_iter, workspace, workspace_bytes,
+                                static_cast<double*>(alpha_out), b_out, info, s);
+    return train_impl<float>(static_cast<const float*>(X), static_cast<const float*>(y), n, d,
+                             kernel, p, C, eps, max_iter, workspace, workspace_bytes,
+                             static_cast<float*>(alpha_out), b_out, info, s);
+  } catch (...) {
+    return fail(LSSVM_EHIP, "internal error");
+  }
+}
+
+int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, int64_t d,
+                  int32_t dtype, int32_t kernel, const lssvm_params* kp, const void* X_test,
+                  int64_t n_test, void* workspace, size_t workspace_bytes, void* scores_out,
+                  int32_t* labels_out, void* stream) {
+  try {
+    g_last_error.clear();
+    if (!X_train || !alpha || !X_test || !scores_out)
+      return fail(LSSVM_EINVAL, "NULL array argument");
+    if (!valid_dtype(dtype)) return fail(LSSVM_EINVAL, "unknown dtype %d", (int)dtype);
+    LSSVM_TRY(check_sizes(n, d, 1));
+    if (n_test < 1 || n_test > (int64_t(1) << 22))
+      return fail(LSSVM_EINVAL, "n_test must be in [1, 2^22] (got %lld)", (long long)n_test);
+    LSSVM_TRY(check_kernel_params(kernel, kp));
+    if (!std::isfinite(b)) return fail(LSSVM_EINVAL, "b must be finite");
+    const lssvm_params p = params_or_default(kp);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == LSSVM_F64)
+      return predict_impl<double>(static_cast<const double*>(X_train),
+                                  static_cast<const double*>(alpha), b, n, d, kernel, p,
+                                  static_cast<const double*>(X_test), n_test, workspace,
+                                  workspace_bytes, static_cast<double*>(scores_out), labels_out,
+                                  s);
+    return predict_impl<float>(static_cast<const float*>(X_train),
+                               static_cast<const float*>(alpha), b, n, d, kernel, p,
+                               static_cast<const float*>(X_test), n_test, workspace,
+                               workspace_bytes, static_cast<float*>(scores_out), labels_out, s);
+  } catch (...) {
+    return fail(LSSVM_EHIP, "internal error");
+  }
+}
+
+int lssvm_matvec(const void* X, int64_t n, int64_t d, int32_t dtype, int32_t kernel,
+                 const lssvm_params* kp, double C, const void* p, void* out, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  try {
+    g_last_error.clear();
+    if (!X || !p || !out) return fail(LSSVM_EINVAL, "NULL array argument");
+    if (!valid_dtype(dtype)) return fail(LSSVM_EINVAL, "unknown dtype %d", (int)dtype);
+    LSSVM_TRY(check_sizes(n, d, 2));
+    LSSVM_TRY(check_kernel_params(kernel, kp));
+    if (!(C > 0.0) || !std::isfinite(C)) return fail(LSSVM_EINVAL, "C must be finite and > 0");
+    const lssvm_params pr = params_or_default(kp);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (dtype == LSSVM_F64)
+      return matvec_impl<double>(static_cast<const double*>(X), n, d, kernel, pr, C,
+                                 static_cast<const double*>(p), static_cast<double*>(out),
+                                 workspace, workspace_bytes, s);
+    return matvec_impl<float>(static_cast<const float*>(X), n, d, kernel, pr, C,
+                              static_cast<const float*>(p), static_cast<float*>(out), workspace,
+                              workspace_bytes, s);
+  } catch (...) {
+    return fail(LSSVM_EHIP, "internal error");
+  }
+}
+
+}  // extern "C"

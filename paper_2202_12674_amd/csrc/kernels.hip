@@ -1,0 +1,812 @@
+// gfx950 (MI355X, CDNA4) kernels of the LS-SVM training hot path.
+//
+// a1  k_layout        row-major points -> padded feature-major layout (Sec. III-A)
+// a2  k_norms_q       squared norms, q_i = k(x_i, x_m) and k(x_m, x_m) (Sec. III-C2)
+// a3  k_rhs_init      rhs = ybar - y_m 1 (Eq. (14)), CG start vectors
+// a4  k_tiles         implicit Q~ p (Eq. (16)) on the matrix cores, one tile of the
+//                     upper triangle per workgroup (Sec. III-C1), rows and columns
+//                     accumulated from the same tile
+// a5  k_cg_*          CG vector updates with fixed-order fp64 reductions (Sec. III-B)
+// a6  k_bias          alpha_m and b (Eqs. (11), (15))
+// a7  k_tiles<gen>    decision values sum_j alpha_j k(x_j, x) + b (Eq. (10))
+//
+// Every reduction sums in a fixed order (no floating-point atomics), so the
+// results are bitwise reproducible run to run.
+#include "lssvm_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+namespace lssvm {
+
+namespace {
+
+constexpr int NT = 256;  // threads per block of the vector kernels
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- MFMA ------
+// One matrix-core instruction computes an M x M block D += A B with a
+// contraction depth K. Lane l supplies A[l % M][l / M] and B[l / M][l % M];
+// accumulator element v of lane l is D[row(v, l)][l % M].
+template <typename T> struct Mfma;
+
+template <> struct Mfma<float> {  // v_mfma_f32_32x32x2_f32
+  static constexpr int M = 32, K = 2, NACC = 16;
+  using acc_t = floatx16;
+  __device__ static inline acc_t zero() {
+    acc_t z;
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) z[i] = 0.f;
+    return z;
+  }
+  __device__ static inline acc_t mma(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline int row(int v, int lane) {
+    return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+  }
+};
+
+template <> struct Mfma<double> {  // v_mfma_f64_16x16x4_f64
+  static constexpr int M = 16, K = 4, NACC = 4;
+  using acc_t = doublex4;
+  __device__ static inline acc_t zero() {
+    acc_t z;
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) z[i] = 0.0;
+    return z;
+  }
+  __device__ static inline acc_t mma(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline int row(int v, int lane) { return (lane >> 4) + 4 * v; }
+};
+
+// Workgroup tiling of the contraction: a T x T tile, four waves in a 2 x 2
+// grid, each wave owning a (T/2) x (T/2) block of MFMA accumulators.
+template <typename T> struct TileCfg {
+  static constexpr int BM = TileShape<T>::T;
+  static constexpr int BK = TileShape<T>::BK;
+  static constexpr int WM = BM / 2, WN = BM / 2;
+  static constexpr int PAD = 16 / sizeof(T);  // LDS row padding (one 16-byte vector)
+};
+
+template <typename T> __device__ inline T texp(T x);
+template <> __device__ inline float texp<float>(float x) { return expf(x); }
+template <> __device__ inline double texp<double>(double x) { return exp(x); }
+
+// Kernel value from the inner product g = <x_i, x_j> (and squared norms for RBF).
+template <int KER, typename T>
+__device__ inline T kernel_value(T g, T ni, T nj, T gamma, T coef0, int degree) {
+  if constexpr (KER == KLIN) {
+    return g;
+  } else if constexpr (KER == KPOLY) {
+    const T base = gamma * g + coef0;
+    T r = base;
+    for (int e = 1; e < degree; ++e) r *= base;
+    return r;
+  } else {
+    T dist = ni + nj - T(2) * g;
+    dist = dist > T(0) ? dist : T(0);
+    return texp<T>(-gamma * dist);
+  }
+}
+
+// fp64 kernel value from a dot product and a directly summed squared distance.
+template <int KER>
+__device__ inline double kernel_value64(double dot, double dist, double gamma, double coef0,
+                                        int degree) {
+  if constexpr (KER == KLIN) {
+    return dot;
+  } else if constexpr (KER == KPOLY) {
+    const double base = gamma * dot + coef0;
+    double r = base;
+    for (int e = 1; e < degree; ++e) r *= base;
+    return r;
+  } else {
+    return exp(-gamma * dist);
+  }
+}
+
+// t = J (J + 1) / 2 + I with 0 <= I <= J: enumerates the upper triangle of
+// tiles column by column, so consecutive workgroups share the column panel.
+__device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
+  int64_t j = (int64_t)((sqrt(8.0 * (double)t + 1.0) - 1.0) * 0.5);
+  while ((j + 1) * (j + 2) / 2 <= t) ++j;
+  while (j * (j + 1) / 2 > t) --j;
+  J = j;
+  I = t - j * (j + 1) / 2;
+}
+
+// Block-wide sum of one double per thread; every thread gets the result.
+// Fixed reduction order, so every block that sums the same values agrees.
+__device__ inline double block_sum(double v, double* sh) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) sh[w] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) s += sh[i];
+  return s;
+}
+
+// Sum of the nb per-block partials written by the previous kernel.
+__device__ inline double sum_partials(const double* bp, int64_t nb, double* sh) {
+  double v = 0.0;
+  for (int64_t i = threadIdx.x; i < nb; i += blockDim.x) v += bp[i];
+  return block_sum(v, sh);
+}
+
+// ------------------------------------------------------------- a1 layout ----
+// 64 points x 64 features per block, transposed through LDS so that both the
+// row-major reads and the feature-major writes are coalesced. Zero fill
+// beyond n points and d features.
+template <typename T>
+__global__ __launch_bounds__(256) void k_layout(const T* __restrict__ X, int64_t n, int64_t d,
+                                                T* __restrict__ Xt, int64_t ld, int64_t d_pad,
+                                                int* __restrict__ flags) {
+  __shared__ T tile[64][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t i0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
+  bool bad = false;
+  for (int r = ty; r < 64; r += 4) {
+    const int64_t i = i0 + r, k = k0 + tx;
+    T v = T(0);
+    if (i < n && k < d) {
+      v = X[i * d + k];
+      bad |= !__builtin_isfinite(v);
+    }
+    tile[r][tx] = v;
+  }
+  __syncthreads();
+  for (int r = ty; r < 64; r += 4) {
+    const int64_t k = k0 + r, i = i0 + tx;
+    if (k < d_pad && i < ld) Xt[k * ld + i] = tile[tx][r];
+  }
+  if (bad) flags[F_NONFINITE] = 1;
+}
+
+// ----------------------------------------------------------- a2 norms, q ----
+// One thread per point: ||x_i||^2 and, if a pivot m is given, the cached
+// q_i = k(x_i, x_m) for i < N (zero beyond) and k(x_m, x_m). fp64 sums.
+template <typename T, int KER>
+__global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xt, int64_t ld, int64_t d,
+                                                 int64_t m, int64_t N, double gamma, double coef0,
+                                                 int degree, T* __restrict__ norms,
+                                                 T* __restrict__ qT, double* __restrict__ q64,
+                                                 double* __restrict__ scal) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i >= ld) return;
+  double nrm = 0.0, dot = 0.0, dist = 0.0;
+  if (m >= 0) {
+#pragma unroll 4
+    for (int64_t k = 0; k < d; ++k) {
+      const double xv = (double)Xt[k * ld + i];
+      const double xm = (double)Xt[k * ld + m];
+      nrm += xv * xv;
+      dot += xv * xm;
+      const double df = xv - xm;
+      dist += df * df;
+    }
+  } else {
+#pragma unroll 4
+    for (int64_t k = 0; k < d; ++k) {
+      const double xv = (double)Xt[k * ld + i];
+      nrm += xv * xv;
+    }
+  }
+  norms[i] = (T)nrm;
+  if (m >= 0) {
+    const double kv = kernel_value64<KER>(dot, dist, gamma, coef0, degree);
+    const double qv = i < N ? kv : 0.0;
+    q64[i] = qv;
+    qT[i] = (T)qv;
+    if (i == m) scal[S_KMM] = kv;
+  }
+}
+
+// ---------------------------------------------------------- a4 tiles --------
+// One T x T tile of the pairwise contraction G = X_I X_J^T per workgroup,
+// feature blocks of BK staged global -> registers -> LDS (double-buffered)
+// and fed to the matrix cores. The epilogue turns G into kernel values and
+// then into Q~ entries (symmetric mode) and folds them into row sums
+// (times p_j) and, off the diagonal, column sums (times p_i), so that each
+// off-diagonal tile serves both triangles. Row and column sums are reduced
+// across lanes and waves in a fixed order and written as fp64 partials,
+// one slot per tile column (rows of block I) or tile row (rows of block J).
+template <typename T, bool SYM, int KER>
+__global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
+  using MF = Mfma<T>;
+  using C = TileCfg<T>;
+  constexpr int BM = C::BM, BK = C::BK, LDP = BM + C::PAD;
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int VPR = BM / VEC;             // 16-byte vectors per panel row
+  constexpr int LOADS = BK * VPR / 256;     // vectors per thread per panel
+  static_assert(BK * VPR % 256 == 0, "panel must split evenly over 256 threads");
+  constexpr int RB = C::WM / MF::M, CB = C::WN / MF::M;
+  constexpr int WAVES_N = BM / C::WN, WAVES_M = BM / C::WM;
+  static_assert(WAVES_M * WAVES_N == 4, "four waves per workgroup");
+  typedef T vec_t __attribute__((ext_vector_type(VEC)));
+
+  __shared__ __attribute__((aligned(16))) T As[2][BK][LDP];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BK][LDP];
+  __shared__ T red_r[WAVES_N][BM];
+  __shared__ T red_c[WAVES_M][BM];
+
+  int64_t I, J;
+  if constexpr (SYM) {
+    tri_index((int64_t)blockIdx.x, I, J);
+  } else {
+    I = (int64_t)blockIdx.x / a.nTc;
+    J = (int64_t)blockIdx.x % a.nTc;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const T* __restrict__ Ap = a.A + I * BM;
+  const T* __restrict__ Bp = a.B + J * BM;
+
+  vec_t ra[LOADS], rb[LOADS];
+  auto gload = [&](int64_t kb) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int v = tid + 256 * u;
+      const int row = v / VPR, cv = v % VPR;
+      const int64_t k = kb * BK + row;
+      ra[u] = *reinterpret_cast<const vec_t*>(Ap + k * a.lda + cv * VEC);
+      rb[u] = *reinterpret_cast<const vec_t*>(Bp + k * a.ldb + cv * VEC);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int v = tid + 256 * u;
+      const int row = v / VPR, cv = v % VPR;
+      *reinterpret_cast<vec_t*>(&As[buf][row][cv * VEC]) = ra[u];
+      *reinterpret_cast<vec_t*>(&Bs[buf][row][cv * VEC]) = rb[u];
+    }
+  };
+
+  typename MF::acc_t acc[RB][CB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int j = 0; j < CB; ++j) acc[i][j] = MF::zero();
+
+  const int cl = lane % MF::M;   // column of this lane inside an MFMA block
+  const int kl = lane / MF::M;   // contraction index of this lane
+
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int64_t kb = 0; kb < a.nkb; ++kb) {
+    const int cur = (int)(kb & 1);
+    if (kb + 1 < a.nkb) gload(kb + 1);
+#pragma unroll
+    for (int kk = 0; kk < BK / MF::K; ++kk) {
+      const int kr = kk * MF::K + kl;
+      T av[RB], bv[CB];
+#pragma unroll
+      for (int i = 0; i < RB; ++i) av[i] = As[cur][kr][wm * C::WM + i * MF::M + cl];
+#pragma unroll
+      for (int j = 0; j < CB; ++j) bv[j] = Bs[cur][kr][wn * C::WN + j * MF::M + cl];
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) acc[i][j] = MF::mma(av[i], bv[j], acc[i][j]);
+    }
+    if (kb + 1 < a.nkb) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: kernel values, Q~ entries, row and column sums
+  const bool diag = SYM && (I == J);
+  int64_t gj[CB];
+  T nBj[CB], qBj[CB], pBj[CB];
+#pragma unroll
+  for (int j = 0; j < CB; ++j) {
+    gj[j] = J * BM + wn * C::WN + j * MF::M + cl;
+    nBj[j] = (KER == KRBF) ? a.nB[gj[j]] : T(0);
+    qBj[j] = SYM ? a.qB[gj[j]] : T(0);
+    pBj[j] = a.pB[gj[j]];
+  }
+  T rs[RB][MF::NACC];
+  T cs[CB];
+#pragma unroll
+  for (int j = 0; j < CB; ++j) cs[j] = T(0);
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+#pragma unroll
+    for (int v = 0; v < MF::NACC; ++v) {
+      const int lr = wm * C::WM + i * MF::M + MF::row(v, lane);
+      const int64_t gi = I * BM + lr;
+      const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
+      const T qAi = SYM ? a.qA[gi] : T(0);
+      const T pAi = SYM ? a.pA[gi] : T(0);
+      T rsum = T(0);
+#pragma unroll
+      for (int j = 0; j < CB; ++j) {
+        const T kv = kernel_value<KER, T>(acc[i][j][v], nAi, nBj[j], a.gamma, a.coef0, a.degree);
+        if constexpr (SYM) {
+          T qt = kv - qAi - qBj[j] + a.qmm;
+          if (gi == gj[j]) qt += a.invC;
+          rsum += qt * pBj[j];
+          cs[j] += qt * pAi;
+        } else {
+          rsum += kv * pBj[j];
+        }
+      }
+      rs[i][v] = rsum;
+    }
+  }
+  // lanes that share a row differ only in the bits of cl
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int v = 0; v < MF::NACC; ++v)
+#pragma unroll
+      for (int off = 1; off < MF::M; off <<= 1) rs[i][v] += __shfl_xor(rs[i][v], off);
+  // lanes that share a column differ only in the bits above cl
+#pragma unroll
+  for (int j = 0; j < CB; ++j)
+#pragma unroll
+    for (int off = MF::M; off < 64; off <<= 1) cs[j] += __shfl_xor(cs[j], off);
+
+  if (cl == 0) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int v = 0; v < MF::NACC; ++v)
+        red_r[wn][wm * C::WM + i * MF::M + MF::row(v, lane)] = rs[i][v];
+  }
+  if (SYM && kl == 0) {
+#pragma unroll
+    for (int j = 0; j < CB; ++j) red_c[wm][wn * C::WN + j * MF::M + cl] = cs[j];
+  }
+  __syncthreads();
+  if (tid < BM) {
+    T s = T(0);
+#pragma unroll
+    for (int w = 0; w < WAVES_N; ++w) s += red_r[w][tid];
+    a.part[J * a.part_ld + I * BM + tid] = (double)s;
+  } else if (SYM && !diag && tid < 2 * BM) {
+    const int c = tid - BM;
+    T s = T(0);
+#pragma unroll
+    for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
+    a.part[I * a.part_ld + J * BM + c] = (double)s;
+  }
+}
+
+// ------------------------------------------------------------- a3 rhs -------
+template <typename T>
+__global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64_t N, int64_t NP,
+                                                  double* rhs, double* x, double* r, double* dir,
+                                                  T* pT, double* bpart, int* flags) {
+  __shared__ double sh[NT / 64];
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  const double ym = (double)y[N];
+  double v = 0.0;
+  if (i < N) {
+    const double yi = (double)y[i];
+    if (!(yi == 1.0 || yi == -1.0)) flags[F_BADLABEL] = 1;
+    v = yi - ym;
+  }
+  if (i == 0 && !(ym == 1.0 || ym == -1.0)) flags[F_BADLABEL] = 1;
+  if (i < NP) {
+    rhs[i] = v;
+    x[i] = 0.0;
+    r[i] = v;
+    dir[i] = v;
+    pT[i] = (T)v;
+  }
+  const double s = block_sum(v * v, sh);
+  if (threadIdx.x == 0) bpart[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int64_t nb,
+                                                       double* scal) {
+  __shared__ double sh[NT / 64];
+  const double s = sum_partials(bpart, nb, sh);
+  if (threadIdx.x == 0) {
+    scal[S_DELTA0] = s;
+    scal[S_DHIST + 0] = s;
+    scal[S_STATUS + 0] = s;
+    scal[S_STATUS + 1] = 0.0;
+    scal[S_STATUS + 2] = 0.0;
+    scal[S_STATUS + 3] = 0.0;
+  }
+}
+
+// ------------------------------------------------------------- a5 CG --------
+// q = Q~ d from the tile partials (masked beyond N) and the block partials of d^T q.
+__global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ part, int64_t nslots,
+                                                   int64_t NP, int64_t N,
+                                                   const double* __restrict__ dir, double* qv,
+                                                   double* bpart) {
+  __shared__ double sh[NT / 64];
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  double prod = 0.0;
+  if (i < NP) {
+    double s = 0.0;
+    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
+    if (i >= N) s = 0.0;
+    qv[i] = s;
+    prod = dir[i] * s;
+  }
+  const double t = block_sum(prod, sh);
+  if (threadIdx.x == 0) bpart[blockIdx.x] = t;
+}
+
+// x += a d and r -= a q (or, when the residual is about to be recomputed,
+// x += a d and the direction buffer receives x for that product).
+template <typename T>
+__global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __restrict__ bp_in,
+                                                   int64_t nb, double* scal, int par,
+                                                   const double* __restrict__ dir,
+                                                   const double* __restrict__ qv, double* x,
+                                                   double* r, T* pT, double* bp_out, int64_t NP) {
+  __shared__ double sh[NT / 64];
+  const double gam = sum_partials(bp_in, nb, sh);
+  const double delta = scal[S_DHIST + par];
+  const double alpha = delta / gam;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    scal[S_ALPHA] = alpha;
+    scal[S_GAMMA] = gam;
+  }
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  double v = 0.0;
+  if (i < NP) {
+    const double xi = x[i] + alpha * dir[i];
+    x[i] = xi;
+    if (x_only) {
+      pT[i] = (T)xi;
+    } else {
+      const double ri = r[i] - alpha * qv[i];
+      r[i] = ri;
+      v = ri * ri;
+    }
+  }
+  if (!x_only) {
+    const double t = block_sum(v, sh);
+    if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+  }
+}
+
+// r = rhs - Q~ x from the tile partials, and the block partials of r^T r.
+__global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part,
+                                                     int64_t nslots, int64_t NP, int64_t N,
+                                                     const double* __restrict__ rhs, double* r,
+                                                     double* bp_out) {
+  __shared__ double sh[NT / 64];
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  double v = 0.0;
+  if (i < NP) {
+    double s = 0.0;
+    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
+    const double ri = i < N ? rhs[i] - s : 0.0;
+    r[i] = ri;
+    v = ri * ri;
+  }
+  const double t = block_sum(v, sh);
+  if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+}
+
+// ||rhs - Q~ x||^2 partials without touching r (final report only).
+__global__ __launch_bounds__(256) void k_true_residual(const double* __restrict__ part,
+                                                       int64_t nslots, int64_t NP, int64_t N,
+                                                       const double* __restrict__ rhs,
+                                                       double* bp_out) {
+  __shared__ double sh[NT / 64];
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  double v = 0.0;
+  if (i < N) {
+    double s = 0.0;
+    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
+    const double ri = rhs[i] - s;
+    v = ri * ri;
+  }
+  const double t = block_sum(v, sh);
+  if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+}
+
+// beta = r^T r (new) / r^T r (old); d = r + beta d; the direction is also
+// written in the point dtype for the next product.
+template <typename T>
+__global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__ bp_in, int64_t nb,
+                                                      double* scal, int par, int64_t iter,
+                                                      const double* __restrict__ r, double* dir,
+                                                      T* pT, int64_t NP) {
+  __shared__ double sh[NT / 64];
+  const double dnew = sum_partials(bp_in, nb, sh);
+  const double dold = scal[S_DHIST + par];
+  const double beta = dnew / dold;
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i < NP) {
+    const double di = r[i] + beta * dir[i];
+    dir[i] = di;
+    pT[i] = (T)di;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    scal[S_DHIST + (par ^ 1)] = dnew;
+    scal[S_STATUS + 0] = dnew;
+    scal[S_STATUS + 1] = scal[S_GAMMA];
+    scal[S_STATUS + 2] = scal[S_ALPHA];
+    scal[S_STATUS + 3] = (double)iter;
+  }
+}
+
+// ------------------------------------------------------------- a6 bias ------
+// alpha = [x, -sum x] (last row of Eq. (11)); b = y_m + Q_mm sum x - q^T x (Eq. (15)).
+template <typename T>
+__global__ __launch_bounds__(1024) void k_bias(const double* __restrict__ x,
+                                               const double* __restrict__ q64, int64_t N,
+                                               const T* __restrict__ y, double* scal, double invC,
+                                               T* __restrict__ alpha_out) {
+  __shared__ double sh[1024 / 64];
+  double sx = 0.0, sqx = 0.0;
+  for (int64_t i = threadIdx.x; i < N; i += blockDim.x) {
+    const double xi = x[i];
+    sx += xi;
+    sqx += q64[i] * xi;
+    alpha_out[i] = (T)xi;
+  }
+  sx = block_sum(sx, sh);
+  sqx = block_sum(sqx, sh);
+  if (threadIdx.x == 0) {
+    alpha_out[N] = (T)(-sx);
+    const double qmm = scal[S_KMM] + invC;
+    scal[S_B] = (double)y[N] + qmm * sx - sqx;
+  }
+}
+
+template <typename T>
+__global__ void k_single_point(const T* __restrict__ y, T* __restrict__ alpha_out, double* scal,
+                               int* flags) {
+  if (threadIdx.x == 0) {
+    const double y0 = (double)y[0];
+    if (!(y0 == 1.0 || y0 == -1.0)) flags[F_BADLABEL] = 1;
+    alpha_out[0] = T(0);
+    scal[S_B] = y0;
+  }
+}
+
+// ---------------------------------------------------------- misc vectors ----
+template <typename T>
+__global__ __launch_bounds__(256) void k_pad_vec(const T* __restrict__ src, int64_t len,
+                                                 T* __restrict__ dst, int64_t len_pad) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i < len_pad) dst[i] = i < len ? src[i] : T(0);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part, int64_t nslots,
+                                                int64_t NP, int64_t N, T* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i < N) {
+    double s = 0.0;
+    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
+    out[i] = (T)s;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_predict_finish(const double* __restrict__ part,
+                                                        int64_t nslots, int64_t ld, int64_t n_test,
+                                                        double b, T* __restrict__ scores,
+                                                        int32_t* __restrict__ labels) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i < n_test) {
+    double s = b;
+    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * ld + i];
+    scores[i] = (T)s;
+    if (labels) labels[i] = s > 0.0 ? 1 : -1;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_cast_vec(const double* __restrict__ src,
+                                                  T* __restrict__ dst, int64_t len) {
+  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (i < len) dst[i] = (T)src[i];
+}
+
+__global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t nb, double* scal,
+                                                    int slot) {
+  __shared__ double sh[NT / 64];
+  const double s = sum_partials(bpart, nb, sh);
+  if (threadIdx.x == 0) scal[slot] = s;
+}
+
+inline unsigned blocks_for(int64_t n) { return (unsigned)((n + NT - 1) / NT); }
+
+}  // namespace
+
+// ------------------------------------------------------------- launchers ----
+
+template <typename T>
+hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
+                         int* flags, hipStream_t s) {
+  dim3 grid((unsigned)(ld / 64), (unsigned)((d_pad + 63) / 64));
+  hipLaunchKernelGGL(k_layout<T>, grid, dim3(256), 0, s, X, n, d, Xt, ld, d_pad, flags);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d, int64_t m, int64_t N, int kernel,
+                          double gamma, double coef0, int degree, T* norms, T* qT, double* q64,
+                          double* scal, hipStream_t s) {
+  const unsigned g = blocks_for(ld);
+  switch (kernel) {
+    case KLIN:
+      hipLaunchKernelGGL((k_norms_q<T, KLIN>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
+                         coef0, degree, norms, qT, q64, scal);
+      break;
+    case KPOLY:
+      hipLaunchKernelGGL((k_norms_q<T, KPOLY>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
+                         coef0, degree, norms, qT, q64, scal);
+      break;
+    default:
+      hipLaunchKernelGGL((k_norms_q<T, KRBF>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
+                         coef0, degree, norms, qT, q64, scal);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s) {
+  dim3 grid((unsigned)ntiles_1d);
+  switch (kernel) {
+    case KLIN: hipLaunchKernelGGL((k_tiles<T, true, KLIN>), grid, dim3(256), 0, s, a); break;
+    case KPOLY: hipLaunchKernelGGL((k_tiles<T, true, KPOLY>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_tiles<T, true, KRBF>), grid, dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s) {
+  dim3 grid((unsigned)(nTr * a.nTc));
+  switch (kernel) {
+    case KLIN: hipLaunchKernelGGL((k_tiles<T, false, KLIN>), grid, dim3(256), 0, s, a); break;
+    case KPOLY: hipLaunchKernelGGL((k_tiles<T, false, KPOLY>), grid, dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((k_tiles<T, false, KRBF>), grid, dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
+                           double* dir, T* pT, double* bpart, int* flags, hipStream_t s) {
+  hipLaunchKernelGGL(k_rhs_init<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
+                     dir, pT, bpart, flags);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish_delta0, dim3(1), dim3(NT), 0, s, bpart, nb, scal);
+  return hipGetLastError();
+}
+
+hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                            const double* dir, double* qv, double* bpart, hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_gather, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N, dir,
+                     qv, bpart);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
+                            const double* dir, const double* qv, double* x, double* r, T* pT,
+                            double* bp_out, int64_t NP, hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_update<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, x_only, bp_in, nb,
+                     scal, par, dir, qv, x, r, pT, bp_out, NP);
+  return hipGetLastError();
+}
+
+hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                              const double* rhs, double* r, double* bp_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_residual, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N,
+                     rhs, r, bp_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                                const double* rhs, double* bp_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_true_residual, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N,
+                     rhs, bp_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
+                               int64_t iter, const double* r, double* dir, T* pT, int64_t NP,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_direction<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, bp_in, nb, scal,
+                     par, iter, r, dir, pT, NP);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_bias(const double* x, const double* q64, int64_t N, const T* y, double* scal,
+                       double invC, T* alpha_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_bias<T>, dim3(1), dim3(1024), 0, s, x, q64, N, y, scal, invC, alpha_out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_single_point(const T* y, T* alpha_out, double* scal, int* flags,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_single_point<T>, dim3(1), dim3(64), 0, s, y, alpha_out, scal, flags);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hipStream_t s) {
+  hipLaunchKernelGGL(k_pad_vec<T>, dim3(blocks_for(len_pad)), dim3(NT), 0, s, src, len, dst,
+                     len_pad);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_mv_out(const double* part, int64_t nslots, int64_t NP, int64_t N, T* out,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_mv_out<T>, dim3(blocks_for(N)), dim3(NT), 0, s, part, nslots, NP, N, out);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
+                                 double b, T* scores, int32_t* labels, hipStream_t s) {
+  hipLaunchKernelGGL(k_predict_finish<T>, dim3(blocks_for(n_test)), dim3(NT), 0, s, part, nslots,
+                     ld, n_test, b, scores, labels);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_cast_vec(const double* src, T* dst, int64_t len, hipStream_t s) {
+  hipLaunchKernelGGL(k_cast_vec<T>, dim3(blocks_for(len)), dim3(NT), 0, s, src, dst, len);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int slot,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(k_finish_sum, dim3(1), dim3(NT), 0, s, bpart, nb, scal, slot);
+  return hipGetLastError();
+}
+
+#define LSSVM_INSTANTIATE(T)                                                                      \
+  template hipError_t launch_layout<T>(const T*, int64_t, int64_t, T*, int64_t, int64_t, int*,    \
+                                       hipStream_t);                                              \
+  template hipError_t launch_norms_q<T>(const T*, int64_t, int64_t, int64_t, int64_t, int,        \
+                                        double, double, int, T*, T*, double*, double*,            \
+                                        hipStream_t);                                             \
+  template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
+  template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
+  template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
+                                         double*, T*, double*, int*, hipStream_t);                \
+  template hipError_t launch_cg_update<T>(int, const double*, int64_t, double*, int,              \
+                                          const double*, const double*, double*, double*, T*,     \
+                                          double*, int64_t, hipStream_t);                         \
+  template hipError_t launch_cg_direction<T>(const double*, int64_t, double*, int, int64_t,       \
+                                             const double*, double*, T*, int64_t, hipStream_t);   \
+  template hipError_t launch_bias<T>(const double*, const double*, int64_t, const T*, double*,    \
+                                     double, T*, hipStream_t);                                    \
+  template hipError_t launch_single_point<T>(const T*, T*, double*, int*, hipStream_t);           \
+  template hipError_t launch_pad_vec<T>(const T*, int64_t, T*, int64_t, hipStream_t);             \
+  template hipError_t launch_mv_out<T>(const double*, int64_t, int64_t, int64_t, T*,              \
+                                       hipStream_t);                                              \
+  template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
+                                               T*, int32_t*, hipStream_t);                        \
+  template hipError_t launch_cast_vec<T>(const double*, T*, int64_t, hipStream_t);
+
+LSSVM_INSTANTIATE(float)
+LSSVM_INSTANTIATE(double)
+
+}  // namespace lssvm

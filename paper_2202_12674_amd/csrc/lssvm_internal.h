@@ -1,0 +1,103 @@
+// Internal interface between the host runtime (api.cpp) and the gfx950
+// kernels (kernels.hip). Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace lssvm {
+
+enum Kern : int { KLIN = 0, KPOLY = 1, KRBF = 2 };
+
+// Points per tile edge and features per staged block, per element type.
+// The symmetric schedule needs square tiles.
+template <typename T> struct TileShape;
+template <> struct TileShape<float> { static constexpr int T = 128, BK = 16; };
+template <> struct TileShape<double> { static constexpr int T = 128, BK = 8; };
+
+// Slots of the small fp64 scalar area in the workspace.
+enum Scalar : int {
+  S_KMM = 0,     // k(x_m, x_m)
+  S_DHIST = 1,   // r^T r of the current iterate, double-buffered: [1], [2]
+  S_DELTA0 = 3,  // r0^T r0
+  S_B = 4,       // bias
+  S_ALPHA = 5,   // CG step length of the last update
+  S_GAMMA = 6,   // curvature d^T Q~ d of the last update
+  S_TRUE = 7,    // ||rhs - Q~ x||^2 (final report)
+  S_STATUS = 8,  // 4 doubles copied to the host each iteration:
+                 // [0] r^T r, [1] curvature, [2] step length, [3] iteration tag
+  S_COUNT = 16
+};
+
+// Flags raised by kernels (int32 each).
+enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
+
+template <typename T>
+struct TileArgs {
+  const T* A;    // feature-major row-point panel source, A[k * lda + i]
+  const T* B;    // feature-major column-point panel source
+  int64_t lda, ldb;
+  int64_t nkb;   // feature blocks of BK
+  const T* nA;   // squared norms of row points (RBF)
+  const T* nB;   // squared norms of column points (RBF)
+  const T* qA;   // q_i = k(x_i, x_m) (symmetric mode), zero beyond N
+  const T* qB;
+  const T* pA;   // vector multiplied into column sums (symmetric mode)
+  const T* pB;   // vector multiplied into row sums (p, or alpha in predict)
+  T gamma, coef0, qmm, invC;
+  int degree;
+  int64_t nTc;   // column tiles (general mode)
+  double* part;  // partial sums, part[slot * part_ld + row]
+  int64_t part_ld;
+};
+
+template <typename T>
+hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
+                         int* flags, hipStream_t s);
+template <typename T>
+hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d, int64_t m, int64_t N, int kernel,
+                          double gamma, double coef0, int degree, T* norms, T* qT, double* q64,
+                          double* scal, hipStream_t s);
+template <typename T>
+hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s);
+template <typename T>
+hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
+template <typename T>
+hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
+                           double* dir, T* pT, double* bpart, int* flags, hipStream_t s);
+hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, hipStream_t s);
+hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                            const double* dir, double* qv, double* bpart, hipStream_t s);
+template <typename T>
+hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
+                            const double* dir, const double* qv, double* x, double* r, T* pT,
+                            double* bp_out, int64_t NP, hipStream_t s);
+hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                              const double* rhs, double* r, double* bp_out, hipStream_t s);
+template <typename T>
+hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
+                               int64_t iter, const double* r, double* dir, T* pT, int64_t NP,
+                               hipStream_t s);
+template <typename T>
+hipError_t launch_bias(const double* x, const double* q64, int64_t N, const T* y, double* scal,
+                       double invC, T* alpha_out, hipStream_t s);
+template <typename T>
+hipError_t launch_single_point(const T* y, T* alpha_out, double* scal, int* flags, hipStream_t s);
+template <typename T>
+hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hipStream_t s);
+template <typename T>
+hipError_t launch_mv_out(const double* part, int64_t nslots, int64_t NP, int64_t N, T* out,
+                         hipStream_t s);
+template <typename T>
+hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
+                                 double b, T* scores, int32_t* labels, hipStream_t s);
+template <typename T>
+hipError_t launch_cast_vec(const double* src, T* dst, int64_t len, hipStream_t s);
+hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int slot,
+                             hipStream_t s);
+hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+                                const double* rhs, double* bp_out, hipStream_t s);
+
+}  // namespace lssvm

@@ -1,0 +1,146 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+declared in include/lssvm.h, sizes workspaces, and rejects bad arguments on
+the host before any GPU work (so these paths run here without a device)."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2202_12674_amd as P
+from paper_2202_12674_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lssvm.h")
+
+FAKE = ctypes.c_void_p(4096)          # never dereferenced: validation fails first
+ALIGNED_WS = ctypes.c_void_p(1 << 20)
+
+
+def header_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(lssvm_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_function():
+    L = P.lib()
+    names = header_functions()
+    assert {"lssvm_train", "lssvm_predict", "lssvm_matvec", "lssvm_workspace_bytes",
+            "lssvm_predict_workspace_bytes", "lssvm_last_error", "lssvm_tile_size"} <= set(names)
+    for nm in names:
+        assert hasattr(L, nm), nm
+
+
+def test_workspace_sizes():
+    L = P.lib()
+    assert L.lssvm_workspace_bytes(0, 4, 0) == 0
+    assert L.lssvm_workspace_bytes(4, 0, 0) == 0
+    assert L.lssvm_workspace_bytes(4, 4, 7) == 0
+    small = L.lssvm_workspace_bytes(256, 64, 0)
+    assert small > 256 * 64 * 8
+    # fp32 layout of 32768 x 4096 points alone is 512 MiB
+    assert L.lssvm_workspace_bytes(32768, 4096, 1) >= 32768 * 4096 * 4
+    assert L.lssvm_workspace_bytes(1, 1, 1) > 0
+    assert L.lssvm_predict_workspace_bytes(100, 0, 3, 0) == 0
+    assert L.lssvm_predict_workspace_bytes(100, 10, 3, 1) > 100 * 3 * 4
+    assert L.lssvm_tile_size(0) in (64, 128, 256) and L.lssvm_tile_size(1) in (64, 128, 256)
+    assert L.lssvm_tile_size(5) == 0
+
+
+def _train(n=10, d=3, dtype=0, kernel=0, params=None, C=1.0, eps=1e-3, max_iter=0,
+           ws=ALIGNED_WS, ws_bytes=1 << 40, X=FAKE, y=FAKE, alpha=FAKE, b=True, info=None):
+    L = P.lib()
+    bb = ctypes.c_double(0)
+    kp = ctypes.byref(params) if params is not None else None
+    return L.lssvm_train(X, y, n, d, dtype, kernel, kp, C, eps, max_iter, ws, ws_bytes, alpha,
+                         ctypes.byref(bb) if b else None, info, None)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(X=None), "NULL"), (dict(y=None), "NULL"), (dict(alpha=None), "NULL"),
+    (dict(b=False), "NULL"), (dict(n=0), "n must"), (dict(d=0), "d must"),
+    (dict(dtype=2), "dtype"), (dict(kernel=3), "kernel"),
+    (dict(kernel=1), "parameters required"),
+    (dict(kernel=1, params=B.Params(0.0, 1.0, 3)), "gamma"),
+    (dict(kernel=2, params=B.Params(-1.0, 0.0, 1)), "gamma"),
+    (dict(kernel=1, params=B.Params(1.0, 1.0, 0)), "degree"),
+    (dict(kernel=1, params=B.Params(1.0, float("nan"), 2)), "coef0"),
+    (dict(C=0.0), "C must"), (dict(C=float("inf")), "C must"), (dict(C=-1.0), "C must"),
+    (dict(eps=0.0), "eps"), (dict(eps=1.0), "eps"), (dict(eps=float("nan")), "eps"),
+    (dict(max_iter=-1), "max_iter"),
+    (dict(ws=None), "workspace is NULL"), (dict(ws=ctypes.c_void_p(4100)), "aligned"),
+    (dict(ws_bytes=16), "too small"),
+    (dict(n=1 << 23), "too large"), (dict(d=1 << 22), "too large"),
+])
+def test_train_rejects_bad_arguments(kw, msg):
+    code = _train(**kw)
+    assert code == B.EINVAL
+    assert msg in P.last_error()
+
+
+def test_train_history_without_buffer():
+    info = B.Info()
+    info.history_capacity = 5
+    assert _train(info=ctypes.byref(info)) == B.EINVAL
+    assert "history" in P.last_error()
+
+
+def test_predict_rejects_bad_arguments():
+    L = P.lib()
+    kp = B.Params(1.0, 0.0, 1)
+
+    def call(**kw):
+        a = dict(Xtr=FAKE, alpha=FAKE, b=0.0, n=10, d=3, dt=0, k=0, X_test=FAKE, nt=5,
+                 ws=ALIGNED_WS, wsb=1 << 40, scores=FAKE)
+        a.update(kw)
+        return L.lssvm_predict(a["Xtr"], a["alpha"], a["b"], a["n"], a["d"], a["dt"], a["k"],
+                               ctypes.byref(kp), a["X_test"], a["nt"], a["ws"], a["wsb"],
+                               a["scores"], None, None)
+
+    assert call(Xtr=None) == B.EINVAL
+    assert call(scores=None) == B.EINVAL
+    assert call(nt=0) == B.EINVAL and "n_test" in P.last_error()
+    assert call(b=float("nan")) == B.EINVAL
+    assert call(wsb=8) == B.EINVAL and "too small" in P.last_error()
+    assert call(dt=9) == B.EINVAL
+
+
+def test_matvec_rejects_bad_arguments():
+    L = P.lib()
+    kp = B.Params(1.0, 0.0, 1)
+
+    def call(n=10, d=3, C=1.0, p=FAKE, wsb=1 << 40, k=0):
+        return L.lssvm_matvec(FAKE, n, d, 0, k, ctypes.byref(kp), C, p, FAKE, ALIGNED_WS, wsb,
+                              None)
+
+    assert call(n=1) == B.EINVAL and "n must be >= 2" in P.last_error()
+    assert call(C=0.0) == B.EINVAL
+    assert call(p=None) == B.EINVAL
+    assert call(wsb=1) == B.EINVAL
+    assert call(k=7) == B.EINVAL
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    X = torch.zeros(4, 2, dtype=torch.float64)
+    y = torch.ones(4, dtype=torch.float64)
+    with pytest.raises((TypeError, RuntimeError)):
+        P.train(X, y, workspace=torch.zeros(1 << 16, dtype=torch.uint8))
+
+
+def test_last_error_is_thread_local():
+    import threading
+    _train(n=0)
+    seen = {}
+
+    def other():
+        seen["msg"] = P.last_error()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["msg"] == ""
+    assert "n must" in P.last_error()

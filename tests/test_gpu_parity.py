@@ -1,0 +1,349 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Same seeded inputs on both sides. Bars: fp64 matvec 1e-11 and alpha/b 1e-9,
+fp32 matvec 1e-5 and alpha/b 1e-4 (max-norm relative error; b relative to
+max(1, |b|)); predicted labels identical except exact near-ties of the
+oracle's decision value, which are counted and bounded.
+"""
+from __future__ import annotations
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+import synthdata as S
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TOL_MV = {"f64": 1e-11, "f32": 1e-5}
+TOL_ALPHA = {"f64": 1e-9, "f32": 1e-4}
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2202_12674_amd as P
+    P.lib()  # fail loudly if the HIP library is missing
+    return torch, torch.device("cuda:0")
+
+
+def rel_err(a, ref):
+    a = np.asarray(a, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.abs(a - ref).max() / max(np.abs(ref).max(), 1e-300))
+
+
+def spec_of(cfg):
+    return O.KernelSpec(cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+
+
+def kw_of(cfg):
+    return dict(kernel=cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+
+
+def small_cfg(kernel, dtype, n, d, C=1.0, eps=None, flip=0.05):
+    eps = eps if eps is not None else (1e-10 if dtype == "f64" else 1e-5)
+    kw = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=1.0, degree=3),
+              rbf=dict(gamma=1.0 / d))[kernel]
+    return S.Config(f"{kernel}_{dtype}_{n}x{d}", dtype, kernel, n, d, mu=1.0, inf_frac=0.5,
+                    flip_frac=flip, C=C, eps=eps, **kw)
+
+
+_DATA = {}
+
+
+def data_of(cfg):
+    key = (cfg.name, cfg.n, cfg.d, cfg.dtype)
+    if key not in _DATA:
+        X, y, scale = S.make_train(cfg)
+        Xte, yte = S.make_test(cfg, scale)
+        _DATA.clear()
+        _DATA[key] = (X, y, Xte, yte)
+    return _DATA[key]
+
+
+def to_dev(torch, dev, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def labels_match(lab, f_ref, scale_tol):
+    """Labels equal wherever the oracle's decision value is not a near-tie."""
+    f_ref = np.asarray(f_ref)
+    lab_ref = np.where(f_ref > 0, 1, -1)
+    tie = np.abs(f_ref) <= scale_tol * max(1.0, np.abs(f_ref).max())
+    bad = (np.asarray(lab) != lab_ref) & ~tie
+    return int(bad.sum()), int(tie.sum())
+
+
+# ------------------------------------------------------------ matvec --------
+
+SMALL_SHAPES = [(2, 1), (3, 3), (129, 65), (257, 3), (300, 100), (1000, 17)]
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+@pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
+@pytest.mark.parametrize("n,d", SMALL_SHAPES)
+def test_matvec_small_shapes(torch_dev, dtype, kernel, n, d):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=2.0)
+    log(f"matvec {cfg.name}")
+    X, y, _, _ = data_of(cfg)
+    p = S.probe_vector(n - 1, cfg.np_dtype, seed=7)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg))
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    ref = Qt @ p.astype(np.float64)
+    assert rel_err(out.cpu().numpy(), ref) <= TOL_MV[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+@pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
+def test_matvec_unit_vectors_give_columns(torch_dev, dtype, kernel):
+    """Q~ e_j is column j of Q~: checks single entries, the diagonal and padding."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, 300, 40, C=0.5)
+    X, _, _, _ = data_of(cfg)
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    Xd = to_dev(torch, dev, X)
+    N = 299
+    for j in (0, 127, 128, 200, N - 1):
+        e = np.zeros(N, dtype=cfg.np_dtype)
+        e[j] = 1
+        out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt[:, j]) <= TOL_MV[dtype], j
+
+
+@pytest.mark.parametrize("name", ["linear_f64_256x64", "linear_f64_4096x1024"])
+def test_matvec_configs_live_oracle(torch_dev, name):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = S.CONFIGS[name]
+    log(f"matvec {name}")
+    X, y, _, _ = data_of(cfg)
+    N = cfg.n - 1
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    Xd = to_dev(torch, dev, X)
+    for p in (S.probe_vector(N, cfg.np_dtype), O.reduced_rhs(y).astype(cfg.np_dtype)):
+        out = P.matvec(Xd, to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[cfg.dtype]
+
+
+def golden(name):
+    path = os.path.join(GOLDEN, f"{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"golden values for {name} not generated")
+    return np.load(path, allow_pickle=False)
+
+
+@pytest.mark.parametrize("name", list(S.CONFIGS))
+def test_matvec_full_configs_golden(torch_dev, name):
+    """Full-size product with the seeded probe vector against the stored oracle product,
+    plus sampled rows recomputed one by one by the oracle."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = S.CONFIGS[name]
+    g = golden(name)
+    log(f"matvec full {name}")
+    X, y, _, _ = data_of(cfg)
+    assert S.sha256_arrays(X, y) == str(g["hash_train"]), "generator drifted"
+    N = cfg.n - 1
+    p = S.probe_vector(N, cfg.np_dtype)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=cfg.C,
+                   **kw_of(cfg)).cpu().numpy()
+    ref = g["mv_probe"]
+    assert rel_err(out, ref) <= TOL_MV[cfg.dtype]
+    rows = [0, N // 3, N - 1]
+    sampled = O.matvec_rows(X, spec_of(cfg), cfg.C, p, rows)
+    scale = np.abs(ref).max()
+    assert np.abs(out[rows] - sampled).max() / scale <= TOL_MV[cfg.dtype]
+
+
+def test_matvec_deterministic(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("rbf", "f32", 1000, 300)
+    X, _, _, _ = data_of(cfg)
+    Xd = to_dev(torch, dev, X)
+    p = to_dev(torch, dev, S.probe_vector(999, np.float32))
+    a = P.matvec(Xd, p, C=1.0, **kw_of(cfg)).cpu().numpy()
+    b = P.matvec(Xd, p, C=1.0, **kw_of(cfg)).cpu().numpy()
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------------- train --------
+
+def check_train(torch, dev, cfg, ref_alpha, ref_b, ref_iters, X, y, Xte=None, f_te=None):
+    import paper_2202_12674_amd as P
+    res = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=cfg.C, eps=cfg.eps,
+                  max_iter=cfg.max_iter, true_residual=True, **kw_of(cfg))
+    log(f"  {cfg.name}: status {res.status} it {res.iterations} (oracle {ref_iters}) "
+        f"rel {res.rel_residual:.2e} true {res.true_rel_residual:.2e} "
+        f"cg {res.t_cg_ms:.1f} ms")
+    assert res.converged
+    alpha = res.alpha.cpu().numpy().astype(np.float64)
+    ea = rel_err(alpha, ref_alpha)
+    eb = abs(res.b - ref_b) / max(1.0, abs(ref_b))
+    log(f"  alpha err {ea:.2e}, b err {eb:.2e}")
+    assert ea <= TOL_ALPHA[cfg.dtype]
+    assert eb <= TOL_ALPHA[cfg.dtype]
+    if cfg.dtype == "f64":
+        assert abs(res.iterations - ref_iters) <= max(2, ref_iters // 10)
+    else:   # fp32 products perturb the Krylov space: a few more iterations are normal
+        assert res.iterations <= 2 * ref_iters + 10
+    assert abs(alpha.sum()) <= 1e-9 * max(1.0, np.abs(alpha).sum()) * (
+        1 if cfg.dtype == "f64" else 1e4)
+    if Xte is not None:
+        scores, labels = P.predict(to_dev(torch, dev, X), res.alpha, res.b, to_dev(torch, dev, Xte),
+                                   **kw_of(cfg))
+        bad, ties = labels_match(labels.cpu().numpy(), f_te, TOL_ALPHA[cfg.dtype] * 10)
+        log(f"  test labels: {bad} mismatches, {ties} near-ties")
+        assert bad == 0
+    return res
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+@pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
+@pytest.mark.parametrize("n,d", [(2, 3), (130, 7), (600, 50)])
+def test_train_small(torch_dev, dtype, kernel, n, d):
+    torch, dev = torch_dev
+    cfg = small_cfg(kernel, dtype, n, d, C=1.0)
+    X, y, Xte, _ = data_of(cfg)
+    alpha, b, info = O.train(X, y, spec_of(cfg), cfg.C, cfg.eps)
+    f_te = O.decision(X, alpha, b, Xte, spec_of(cfg))
+    check_train(torch, dev, cfg, alpha, b, info["iterations"], X, y, Xte, f_te)
+
+
+def test_train_residual_replacement(torch_dev):
+    """C = 100 needs more than 50 iterations, so the residual is recomputed on the way."""
+    torch, dev = torch_dev
+    cfg = small_cfg("rbf", "f64", 700, 12, C=100.0, eps=1e-9)
+    X, y, Xte, _ = data_of(cfg)
+    alpha, b, info = O.train(X, y, spec_of(cfg), cfg.C, cfg.eps)
+    assert info["iterations"] > 50
+    res = check_train(torch, dev, cfg, alpha, b, info["iterations"], X, y)
+    assert res.n_matvec == res.iterations + res.iterations // 50
+
+
+@pytest.mark.parametrize("name", list(S.CONFIGS))
+def test_train_configs(torch_dev, name):
+    torch, dev = torch_dev
+    cfg = S.CONFIGS[name]
+    g = golden(name)
+    log(f"train {name}")
+    X, y, Xte, _ = data_of(cfg)
+    assert S.sha256_arrays(X, y) == str(g["hash_train"]), "generator drifted"
+    assert S.sha256_arrays(Xte) == str(g["hash_test"]), "generator drifted"
+    check_train(torch, dev, cfg, g["alpha"], float(g["b"]), int(g["iterations"]), X, y, Xte,
+                g["f_test"])
+
+
+# ----------------------------------------------------------- predict --------
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+@pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
+@pytest.mark.parametrize("n,nt,d", [(1, 5, 3), (300, 1, 9), (517, 300, 70)])
+def test_predict_oracle_model(torch_dev, dtype, kernel, n, nt, d):
+    """GPU scores for the oracle's own model equal the oracle's scores."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d)
+    X, y, _, _ = data_of(cfg)
+    Xte = S.make_test(cfg, S.minmax_fit(X), n_test=nt, seed=5)[0] if n > 1 else X[:1] * 0.5
+    Xte = np.ascontiguousarray(np.resize(Xte, (nt, d)).astype(cfg.np_dtype))
+    alpha = np.random.default_rng(3).standard_normal(n).astype(cfg.np_dtype)
+    b = 0.125
+    f_ref, _ = O.predict(X, alpha, b, Xte, spec_of(cfg))
+    scores, labels = P.predict(to_dev(torch, dev, X), to_dev(torch, dev, alpha), b,
+                               to_dev(torch, dev, Xte), **kw_of(cfg))
+    s = scores.cpu().numpy()
+    tol = TOL_MV[dtype]
+    assert np.abs(s - f_ref).max() / max(1.0, np.abs(f_ref).max()) <= tol * 10
+    bad, _ = labels_match(labels.cpu().numpy(), f_ref, tol * 10)
+    assert bad == 0
+
+
+# ----------------------------------------------------- edge / errors --------
+
+def test_train_single_point_and_equal_labels(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    for dt in (torch.float64, torch.float32):
+        X = torch.tensor([[0.5, -0.25]], dtype=dt, device=dev)
+        y = torch.tensor([-1.0], dtype=dt, device=dev)
+        r = P.train(X, y)
+        assert r.converged and r.b == -1.0 and r.alpha.cpu().tolist() == [0.0]
+        X = torch.rand(200, 5, dtype=dt, device=dev)
+        y = torch.ones(200, dtype=dt, device=dev)
+        r = P.train(X, y, kernel="rbf", gamma=0.5)
+        assert r.converged and r.iterations == 0 and r.b == 1.0
+        assert float(r.alpha.abs().max()) == 0.0
+
+
+def test_train_not_converged_and_history(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("rbf", "f64", 400, 10)
+    X, y, _, _ = data_of(cfg)
+    r = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=1.0, eps=1e-12, max_iter=1,
+                history=4, **kw_of(cfg))
+    assert r.status == 1 and not r.converged and r.iterations == 1
+    # outputs hold the first iterate: compare with one oracle CG step
+    Qt, q, Qmm = O.reduced_matrix(X, spec_of(cfg), 1.0)
+    rhs = O.reduced_rhs(y)
+    one = O.solve_cg(lambda v: Qt @ v, rhs, 1e-12, max_iter=1)
+    alpha, b = O.recover(one.x, y, q, Qmm)
+    assert rel_err(r.alpha.cpu().numpy(), alpha) <= 1e-9
+    assert abs(r.b - b) <= 1e-9 * max(1, abs(b))
+    assert r.history[0] == pytest.approx(one.history[0] / float(rhs @ rhs), rel=1e-9)
+
+
+def test_train_rejects_nonfinite_and_bad_labels(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    X = torch.rand(64, 3, dtype=torch.float64, device=dev)
+    y = torch.ones(64, dtype=torch.float64, device=dev)
+    y[::2] = -1
+    Xb = X.clone()
+    Xb[5, 1] = float("nan")
+    with pytest.raises(P.LssvmError) as e:
+        P.train(Xb, y)
+    assert e.value.code == -2
+    yb = y.clone()
+    yb[7] = 0.5
+    with pytest.raises(P.LssvmError) as e:
+        P.train(X, yb)
+    assert e.value.code == -3
+    yb = y.clone()
+    yb[63] = 2.0     # the pivot's label
+    with pytest.raises(P.LssvmError) as e:
+        P.train(X, yb)
+    assert e.value.code == -3
+    Xb = X.clone()
+    Xb[0, 0] = float("inf")
+    with pytest.raises(P.LssvmError) as e:
+        P.predict(X, y, 0.0, Xb)
+    assert e.value.code == -2
+
+
+def test_train_deterministic(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("poly", "f32", 900, 33)
+    X, y, _, _ = data_of(cfg)
+    Xd, yd = to_dev(torch, dev, X), to_dev(torch, dev, y)
+    a = P.train(Xd, yd, C=1.0, eps=1e-5, **kw_of(cfg))
+    b = P.train(Xd, yd, C=1.0, eps=1e-5, **kw_of(cfg))
+    assert a.iterations == b.iterations and a.b == b.b
+    assert torch.equal(a.alpha, b.alpha)
