@@ -51,6 +51,13 @@ def make(name):
     print(f"[{name}] cg {res.iterations} it, conv={res.converged}, "
           f"true rel res {res.true_rel_residual:.3e}, {time.time() - t0:.1f}s", flush=True)
     alpha, b = O.recover(res.x, y, q, Qmm)
+    # the same CG with only the summation order of the product changed: the
+    # spread of the aggregates alpha_m = -sum(alpha~) and b that rounding alone causes
+    h = N // 3
+    res2 = O.solve_cg(lambda v: Qt[:, :h] @ v[:h] + Qt[:, h:] @ v[h:], rhs, cfg.eps, cfg.max_iter)
+    alpha2, b2 = O.recover(res2.x, y, q, Qmm)
+    print(f"[{name}] order spread: alpha {np.abs(alpha2 - alpha).max() / np.abs(alpha).max():.2e}"
+          f" b {abs(b2 - b):.2e} ({res2.iterations} it)", flush=True)
     del Qt
     f_te, lab_te = O.predict(X, alpha, b, Xte, spec)
     f_tr, lab_tr = O.predict(X, alpha, b, X[:1024], spec)
@@ -60,6 +67,7 @@ def make(name):
         hash_test=np.array(S.sha256_arrays(Xte)),
         hash_probe=np.array(S.sha256_arrays(p)),
         alpha=alpha, b=np.float64(b), q=q, Qmm=np.float64(Qmm),
+        alpha_alt_order=alpha2, b_alt_order=np.float64(b2),
         iterations=np.int64(res.iterations), converged=np.bool_(res.converged),
         rel_residual=np.float64(res.rel_residual),
         true_rel_residual=np.float64(res.true_rel_residual),
