@@ -7,7 +7,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <chrono>
+#include <vector>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -37,6 +39,12 @@ int fail(int code, const char* fmt, ...) {
                   __FILE__, __LINE__);                                                   \
   } while (0)
 
+#define LSSVM_TRY(expr)      \
+  do {                       \
+    int rc_ = (expr);        \
+    if (rc_ != LSSVM_OK) return rc_; \
+  } while (0)
+
 constexpr size_t kAlign = 256;
 constexpr int64_t kReplaceEvery = 50;  // residual recomputed every 50th iteration
 
@@ -53,7 +61,7 @@ struct Geometry {
   int64_t n, d, N;  // N = n - 1 unknowns of the reduced system
   int64_t tile, bk;
   int64_t ld;       // points per feature row of the layout (>= n, multiple of tile)
-  int64_t d_pad;    // features, multiple of bk
+  int64_t d_pad;    // features, multiple of 2 bk
   int64_t nT;       // tiles per edge of the reduced system
   int64_t NP;       // nT * tile: padded length of every CG vector
   int64_t nb;       // blocks of 256 over NP
@@ -68,7 +76,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.tile = TileShape<T>::T;
   g.bk = TileShape<T>::BK;
   g.ld = round_up(n, g.tile);
-  g.d_pad = round_up(d, g.bk);
+  g.d_pad = round_up(d, 2 * g.bk);   // an even number of feature blocks (two LDS stages)
   g.nT = (g.N + g.tile - 1) / g.tile;
   g.NP = g.nT * g.tile;
   g.nb = (g.NP + 255) / 256;
@@ -100,8 +108,25 @@ struct TrainWs {
   double *bp0, *bp1;
   double* scal;
   int* flags;
+  uint32_t* order;
   size_t bytes;
 };
+
+inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
+
+// Visit order of the upper-triangle tiles: super-tiles of GROUP x GROUP tiles,
+// column by column; inside a super-tile, column by column. Packed (I << 16) | J.
+std::vector<uint32_t> tile_order(int64_t nT, int group) {
+  std::vector<uint32_t> v;
+  v.reserve((size_t)tri_count(nT));
+  const int64_t g = group > 0 ? group : nT;
+  for (int64_t sj = 0; sj < nT; sj += g)
+    for (int64_t si = 0; si <= sj; si += g)
+      for (int64_t j = sj; j < std::min(nT, sj + g); ++j)
+        for (int64_t i = si; i < std::min(j + 1, si + g); ++i)
+          v.push_back((uint32_t)((i << 16) | j));
+  return v;
+}
 
 template <typename T>
 TrainWs<T> carve_train(const Geometry& g, void* base) {
@@ -122,6 +147,7 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.bp1 = c.take<double>(g.nb + 1);
   w.scal = c.take<double>(S_COUNT);
   w.flags = c.take<int>(F_COUNT);
+  w.order = c.take<uint32_t>(LSSVM_TILE_GROUP > 0 ? tri_count(g.nT) : 0);
   w.bytes = c.off;
   return w;
 }
@@ -268,21 +294,32 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.qmm = (T)(kmm + 1.0 / C);
   a.invC = (T)(1.0 / C);
   a.nTc = g.nT;
+  a.order = LSSVM_TILE_GROUP > 0 ? w.order : nullptr;
   a.part = w.part;
   a.part_ld = g.NP;
   return a;
 }
 
-inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
+// Upload the tile visit order into the workspace (once per call).
+template <typename T>
+int upload_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
+  if (LSSVM_TILE_GROUP <= 0 || g.nT == 0) return LSSVM_OK;
+  const std::vector<uint32_t> v = tile_order(g.nT, LSSVM_TILE_GROUP);
+  LSSVM_HIP(hipMemcpyAsync(w.order, v.data(), v.size() * sizeof(uint32_t),
+                           hipMemcpyHostToDevice, s));
+  LSSVM_HIP(hipStreamSynchronize(s));
+  return LSSVM_OK;
+}
 
 // a1 + a2: layout, norms, q and k_mm; reads back k_mm and the input flags.
 template <typename T>
 int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
                  const lssvm_params& kp, hipStream_t s, double* kmm) {
+  LSSVM_TRY(upload_order<T>(g, w, s));
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
   LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
-  LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d, g.N, g.N, kernel, kp.gamma, kp.coef0, kp.degree,
-                              w.norms, w.qT, w.q64, w.scal, s));
+  LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
+                              kp.degree, w.norms, w.qT, w.q64, w.scal, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_KMM, sizeof(double), hipMemcpyDeviceToHost, s));
@@ -311,11 +348,6 @@ int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
   return LSSVM_OK;
 }
 
-#define LSSVM_TRY(expr)      \
-  do {                       \
-    int rc_ = (expr);        \
-    if (rc_ != LSSVM_OK) return rc_; \
-  } while (0)
 
 template <typename T>
 int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
@@ -486,9 +518,9 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   LSSVM_HIP(launch_layout<T>(Xtr, n, d, w.Xtr, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_layout<T>(Xte, n_test, d, w.Xte, w.ld_te, g.d_pad, w.flags, s));
   if (kernel == LSSVM_RBF) {  // squared norms are only read by the radial kernel
-    LSSVM_HIP(launch_norms_q<T>(w.Xtr, g.ld, d, -1, 0, kernel, kp.gamma, kp.coef0, kp.degree,
-                                w.ntr, nullptr, nullptr, nullptr, s));
-    LSSVM_HIP(launch_norms_q<T>(w.Xte, w.ld_te, d, -1, 0, kernel, kp.gamma, kp.coef0,
+    LSSVM_HIP(launch_norms_q<T>(w.Xtr, g.ld, g.d_pad, -1, 0, kernel, kp.gamma, kp.coef0,
+                                kp.degree, w.ntr, nullptr, nullptr, nullptr, s));
+    LSSVM_HIP(launch_norms_q<T>(w.Xte, w.ld_te, g.d_pad, -1, 0, kernel, kp.gamma, kp.coef0,
                                 kp.degree, w.nte, nullptr, nullptr, nullptr, s));
   }
   LSSVM_HIP(launch_pad_vec<T>(alpha, n, w.alpha, g.ld, s));

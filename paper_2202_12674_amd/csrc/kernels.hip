@@ -1,6 +1,6 @@
 // gfx950 (MI355X, CDNA4) kernels of the LS-SVM training hot path.
 //
-// a1  k_layout        row-major points -> padded feature-major layout (Sec. III-A)
+// a1  k_layout        row-major points -> padded feature-blocked layout (Sec. III-A)
 // a2  k_norms_q       squared norms, q_i = k(x_i, x_m) and k(x_m, x_m) (Sec. III-C2)
 // a3  k_rhs_init      rhs = ybar - y_m 1 (Eq. (14)), CG start vectors
 // a4  k_tiles         implicit Q~ p (Eq. (16)) on the matrix cores, one tile of the
@@ -71,7 +71,9 @@ template <typename T> struct TileCfg {
   static constexpr int BM = TileShape<T>::T;
   static constexpr int BK = TileShape<T>::BK;
   static constexpr int WM = BM / 2, WN = BM / 2;
-  static constexpr int PAD = 16 / sizeof(T);  // LDS row padding (one 16-byte vector)
+  static constexpr int PAD = 16 / sizeof(T);  // LDS row padding: one 16-byte vector,
+                                              // which makes the row pitch 36 banks
+                                              // (conflict-free 16-byte reads)
 };
 
 template <typename T> __device__ inline T texp(T x);
@@ -121,6 +123,10 @@ __device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
   I = t - j * (j + 1) / 2;
 }
 
+// Wait until all of this wave's vector memory operations (including direct
+// global -> LDS loads) have completed: s_waitcnt vmcnt(0), other counters free.
+__device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Block-wide sum of one double per thread; every thread gets the result.
 // Fixed reduction order, so every block that sums the same values agrees.
 __device__ inline double block_sum(double v, double* sh) {
@@ -143,61 +149,65 @@ __device__ inline double sum_partials(const double* bp, int64_t nb, double* sh) 
 }
 
 // ------------------------------------------------------------- a1 layout ----
-// 64 points x 64 features per block, transposed through LDS so that both the
-// row-major reads and the feature-major writes are coalesced. Zero fill
-// beyond n points and d features.
-template <typename T>
+// Panel-major, feature-blocked layout. Points are grouped in panels of TP
+// (the tile edge) and features in blocks of BK; panel pb holds its nkb blocks
+// one after the other, and inside a block each point's BK features are
+// contiguous:
+//   Xb[((pb * nkb + kb) * TP + (i % TP)) * BK + kk] = x_i[kb * BK + kk],  pb = i / TP.
+// A tile therefore streams one contiguous run of memory per panel (few pages,
+// coalesced), and each point's features in a block are contiguous (wide LDS
+// reads). Zero fill beyond n points and d features.
+template <typename T, int BK, int TP>
 __global__ __launch_bounds__(256) void k_layout(const T* __restrict__ X, int64_t n, int64_t d,
-                                                T* __restrict__ Xt, int64_t ld, int64_t d_pad,
+                                                T* __restrict__ Xb, int64_t ld, int64_t nkb,
                                                 int* __restrict__ flags) {
-  __shared__ T tile[64][65];
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  const int64_t i0 = (int64_t)blockIdx.x * 64, k0 = (int64_t)blockIdx.y * 64;
-  bool bad = false;
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t i = i0 + r, k = k0 + tx;
-    T v = T(0);
-    if (i < n && k < d) {
-      v = X[i * d + k];
-      bad |= !__builtin_isfinite(v);
-    }
-    tile[r][tx] = v;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= nkb * ld * BK) return;
+  const int64_t kk = idx % BK;
+  const int64_t r = (idx / BK) % TP;
+  const int64_t kb = (idx / ((int64_t)BK * TP)) % nkb;
+  const int64_t pb = idx / ((int64_t)BK * TP * nkb);
+  const int64_t i = pb * TP + r, k = kb * BK + kk;
+  T v = T(0);
+  if (i < n && k < d) {
+    v = X[i * d + k];
+    if (!__builtin_isfinite(v)) flags[F_NONFINITE] = 1;
   }
-  __syncthreads();
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t k = k0 + r, i = i0 + tx;
-    if (k < d_pad && i < ld) Xt[k * ld + i] = tile[tx][r];
-  }
-  if (bad) flags[F_NONFINITE] = 1;
+  Xb[idx] = v;
 }
 
 // ----------------------------------------------------------- a2 norms, q ----
 // One thread per point: ||x_i||^2 and, if a pivot m is given, the cached
 // q_i = k(x_i, x_m) for i < N (zero beyond) and k(x_m, x_m). fp64 sums.
-template <typename T, int KER>
-__global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xt, int64_t ld, int64_t d,
-                                                 int64_t m, int64_t N, double gamma, double coef0,
-                                                 int degree, T* __restrict__ norms,
+template <typename T, int BK, int TP, int KER>
+__global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64_t ld,
+                                                 int64_t nkb, int64_t m, int64_t N, double gamma,
+                                                 double coef0, int degree, T* __restrict__ norms,
                                                  T* __restrict__ qT, double* __restrict__ q64,
                                                  double* __restrict__ scal) {
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   if (i >= ld) return;
   double nrm = 0.0, dot = 0.0, dist = 0.0;
-  if (m >= 0) {
-#pragma unroll 4
-    for (int64_t k = 0; k < d; ++k) {
-      const double xv = (double)Xt[k * ld + i];
-      const double xm = (double)Xt[k * ld + m];
-      nrm += xv * xv;
-      dot += xv * xm;
-      const double df = xv - xm;
-      dist += df * df;
-    }
-  } else {
-#pragma unroll 4
-    for (int64_t k = 0; k < d; ++k) {
-      const double xv = (double)Xt[k * ld + i];
-      nrm += xv * xv;
+  const T* pi = Xb + ((i / TP) * nkb * TP + i % TP) * BK;   // point i, block 0
+  const T* pm = m >= 0 ? Xb + ((m / TP) * nkb * TP + m % TP) * BK : pi;   // pivot, block 0
+  for (int64_t kb = 0; kb < nkb; ++kb) {
+    const T* xi = pi + kb * TP * BK;            // this point's BK features (padding is 0)
+    if (m >= 0) {
+      const T* xm = pm + kb * TP * BK;
+#pragma unroll
+      for (int kk = 0; kk < BK; ++kk) {
+        const double xv = (double)xi[kk], xw = (double)xm[kk];
+        nrm += xv * xv;
+        dot += xv * xw;
+        const double df = xv - xw;
+        dist += df * df;
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < BK; ++kk) {
+        const double xv = (double)xi[kk];
+        nrm += xv * xv;
+      }
     }
   }
   norms[i] = (T)nrm;
@@ -223,24 +233,50 @@ template <typename T, bool SYM, int KER>
 __global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
   using MF = Mfma<T>;
   using C = TileCfg<T>;
-  constexpr int BM = C::BM, BK = C::BK, LDP = BM + C::PAD;
+  constexpr int BM = C::BM, BK = C::BK;
   constexpr int VEC = 16 / sizeof(T);
-  constexpr int VPR = BM / VEC;             // 16-byte vectors per panel row
-  constexpr int LOADS = BK * VPR / 256;     // vectors per thread per panel
-  static_assert(BK * VPR % 256 == 0, "panel must split evenly over 256 threads");
+  constexpr int CPR = BK / VEC;             // 16-byte chunks per point row of a block
+  static_assert(CPR == 8, "rows of 128 bytes: the XOR swizzle below spans 8 chunks");
+  constexpr int CHUNKS = BM * CPR;          // chunks per panel slice
+  constexpr int LOADS = CHUNKS / 256;       // direct loads per thread per panel
+  static_assert(CHUNKS % 256 == 0, "panel must split evenly over 256 threads");
   constexpr int RB = C::WM / MF::M, CB = C::WN / MF::M;
   constexpr int WAVES_N = BM / C::WN, WAVES_M = BM / C::WM;
   static_assert(WAVES_M * WAVES_N == 4, "four waves per workgroup");
+  // Lane group g = lane / M contracts the features [g * FPG, (g + 1) * FPG) of
+  // each block, one per MFMA step; A and B use the same feature order.
+  constexpr int FPG = BK / MF::K;           // features per lane group and block
+  constexpr int CPG = FPG / VEC;            // chunks per lane group
+  static_assert(FPG % VEC == 0, "lane operands are read in 16-byte chunks");
   typedef T vec_t __attribute__((ext_vector_type(VEC)));
+  typedef __attribute__((address_space(1))) const void* gptr_t;
+  typedef __attribute__((address_space(3))) void* lptr_t;
 
-  __shared__ __attribute__((aligned(16))) T As[2][BK][LDP];
-  __shared__ __attribute__((aligned(16))) T Bs[2][BK][LDP];
+  // LDS: per stage and panel, BM rows of 128 bytes; chunk c of point p sits at
+  // physical chunk p * 8 + (c ^ (p & 7)), so both the lane-linear direct
+  // loads and the 16-byte operand reads hit distinct banks.
+  // one array per stage and panel: with fixed names the compiler can tell the
+  // stage being filled from the stage being read and need not wait in between
+  __shared__ __attribute__((aligned(16))) T As0[CHUNKS * VEC];
+  __shared__ __attribute__((aligned(16))) T As1[CHUNKS * VEC];
+  __shared__ __attribute__((aligned(16))) T Bs0[CHUNKS * VEC];
+  __shared__ __attribute__((aligned(16))) T Bs1[CHUNKS * VEC];
   __shared__ T red_r[WAVES_N][BM];
   __shared__ T red_c[WAVES_M][BM];
 
   int64_t I, J;
   if constexpr (SYM) {
-    tri_index((int64_t)blockIdx.x, I, J);
+    if (a.order) {
+      // workgroup w runs on XCD w % 8: give each XCD a contiguous run of the order
+      const uint32_t G = gridDim.x, w = blockIdx.x;
+      const uint32_t x = w % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
+      const uint32_t slot = x * per + (x < extra ? x : extra) + w / kNumXcd;
+      const uint32_t packed = a.order[slot];
+      I = packed >> 16;
+      J = packed & 0xFFFFu;
+    } else {
+      tri_index((int64_t)blockIdx.x, I, J);
+    }
   } else {
     I = (int64_t)blockIdx.x / a.nTc;
     J = (int64_t)blockIdx.x % a.nTc;
@@ -248,27 +284,29 @@ __global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  const T* __restrict__ Ap = a.A + I * BM;
-  const T* __restrict__ Bp = a.B + J * BM;
+  // panel I is nkb consecutive blocks of BM * BK elements
+  const T* __restrict__ Ap = a.A + I * a.nkb * BM * BK;
+  const T* __restrict__ Bp = a.B + J * a.nkb * BM * BK;
+  constexpr int64_t astride = (int64_t)BM * BK, bstride = (int64_t)BM * BK;
 
-  vec_t ra[LOADS], rb[LOADS];
-  auto gload = [&](int64_t kb) {
+  // Direct global -> LDS loads of block kb into stage buf: instruction u of
+  // wave w fills physical chunks [(4u + w) * 64, +64) lane by lane; each lane
+  // fetches the logical chunk that belongs at its physical slot.
+  int goff[LOADS];   // element offset of this lane's logical chunk inside a slice
+#pragma unroll
+  for (int u = 0; u < LOADS; ++u) {
+    const int P = (u * 4 + wave) * 64 + lane;
+    const int p = P / CPR, c = (P % CPR) ^ (p & 7);
+    goff[u] = (p * CPR + c) * VEC;
+  }
+  auto dload = [&](int64_t kb, T (&sa)[CHUNKS * VEC], T (&sb)[CHUNKS * VEC]) {
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
-      const int v = tid + 256 * u;
-      const int row = v / VPR, cv = v % VPR;
-      const int64_t k = kb * BK + row;
-      ra[u] = *reinterpret_cast<const vec_t*>(Ap + k * a.lda + cv * VEC);
-      rb[u] = *reinterpret_cast<const vec_t*>(Bp + k * a.ldb + cv * VEC);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < LOADS; ++u) {
-      const int v = tid + 256 * u;
-      const int row = v / VPR, cv = v % VPR;
-      *reinterpret_cast<vec_t*>(&As[buf][row][cv * VEC]) = ra[u];
-      *reinterpret_cast<vec_t*>(&Bs[buf][row][cv * VEC]) = rb[u];
+      const int base = (u * 4 + wave) * 64 * VEC;   // wave-uniform LDS element offset
+      __builtin_amdgcn_global_load_lds((gptr_t)(Ap + kb * astride + goff[u]),
+                                       (lptr_t)(&sa[base]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gptr_t)(Bp + kb * bstride + goff[u]),
+                                       (lptr_t)(&sb[base]), 16, 0, 0);
     }
   };
 
@@ -278,29 +316,52 @@ __global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
 #pragma unroll
     for (int j = 0; j < CB; ++j) acc[i][j] = MF::zero();
 
-  const int cl = lane % MF::M;   // column of this lane inside an MFMA block
-  const int kl = lane / MF::M;   // contraction index of this lane
+  const int cl = lane % MF::M;   // point of this lane inside an MFMA block
+  const int kl = lane / MF::M;   // lane group: which features of the block it contracts
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int64_t kb = 0; kb < a.nkb; ++kb) {
-    const int cur = (int)(kb & 1);
-    if (kb + 1 < a.nkb) gload(kb + 1);
+  auto compute = [&](const T (&sa)[CHUNKS * VEC], const T (&sb)[CHUNKS * VEC]) {
+    vec_t av[RB][CPG], bv[CB][CPG];
 #pragma unroll
-    for (int kk = 0; kk < BK / MF::K; ++kk) {
-      const int kr = kk * MF::K + kl;
-      T av[RB], bv[CB];
+    for (int i = 0; i < RB; ++i) {
+      const int p = wm * C::WM + i * MF::M + cl;
 #pragma unroll
-      for (int i = 0; i < RB; ++i) av[i] = As[cur][kr][wm * C::WM + i * MF::M + cl];
+      for (int q = 0; q < CPG; ++q)
+        av[i][q] = *reinterpret_cast<const vec_t*>(
+            &sa[(p * CPR + ((kl * CPG + q) ^ (p & 7))) * VEC]);
+    }
 #pragma unroll
-      for (int j = 0; j < CB; ++j) bv[j] = Bs[cur][kr][wn * C::WN + j * MF::M + cl];
+    for (int j = 0; j < CB; ++j) {
+      const int p = wn * C::WN + j * MF::M + cl;
+#pragma unroll
+      for (int q = 0; q < CPG; ++q)
+        bv[j][q] = *reinterpret_cast<const vec_t*>(
+            &sb[(p * CPR + ((kl * CPG + q) ^ (p & 7))) * VEC]);
+    }
+#pragma unroll
+    for (int kk = 0; kk < FPG; ++kk)
 #pragma unroll
       for (int i = 0; i < RB; ++i)
 #pragma unroll
-        for (int j = 0; j < CB; ++j) acc[i][j] = MF::mma(av[i], bv[j], acc[i][j]);
-    }
-    if (kb + 1 < a.nkb) sstore(cur ^ 1);
+        for (int j = 0; j < CB; ++j)
+          acc[i][j] = MF::mma(av[i][kk / VEC][kk % VEC], bv[j][kk / VEC][kk % VEC], acc[i][j]);
+  };
+
+  // Two stages: while block kb is multiplied out of one stage, block kb + 1
+  // streams into the other. A stage is refilled only after the barrier that
+  // ends the iteration which last read it. The host pads the features to an
+  // even number of blocks, so both halves of the loop body always run.
+  const int64_t nkb = a.nkb;
+  dload(0, As0, Bs0);
+  vm_wait_all();
+  __syncthreads();
+  for (int64_t kb = 0; kb < nkb; kb += 2) {
+    dload(kb + 1, As1, Bs1);
+    compute(As0, Bs0);
+    vm_wait_all();     // this wave's part of block kb + 1 has landed
+    __syncthreads();   // every wave's part has landed; stage 0 is free
+    if (kb + 2 < nkb) dload(kb + 2, As0, Bs0);
+    compute(As1, Bs1);
+    vm_wait_all();
     __syncthreads();
   }
 
@@ -632,28 +693,32 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + NT - 1) / NT); }
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
                          int* flags, hipStream_t s) {
-  dim3 grid((unsigned)(ld / 64), (unsigned)((d_pad + 63) / 64));
-  hipLaunchKernelGGL(k_layout<T>, grid, dim3(256), 0, s, X, n, d, Xt, ld, d_pad, flags);
+  constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
+  const int64_t total = d_pad * ld;
+  hipLaunchKernelGGL((k_layout<T, BK, TP>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                     s, X, n, d, Xt, ld, d_pad / BK, flags);
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d, int64_t m, int64_t N, int kernel,
-                          double gamma, double coef0, int degree, T* norms, T* qT, double* q64,
-                          double* scal, hipStream_t s) {
+hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int64_t N,
+                          int kernel, double gamma, double coef0, int degree, T* norms, T* qT,
+                          double* q64, double* scal, hipStream_t s) {
+  constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
+  const int64_t nkb = d_pad / BK;
   const unsigned g = blocks_for(ld);
   switch (kernel) {
     case KLIN:
-      hipLaunchKernelGGL((k_norms_q<T, KLIN>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
-                         coef0, degree, norms, qT, q64, scal);
+      hipLaunchKernelGGL((k_norms_q<T, BK, TP, KLIN>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
+                         gamma, coef0, degree, norms, qT, q64, scal);
       break;
     case KPOLY:
-      hipLaunchKernelGGL((k_norms_q<T, KPOLY>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
-                         coef0, degree, norms, qT, q64, scal);
+      hipLaunchKernelGGL((k_norms_q<T, BK, TP, KPOLY>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
+                         gamma, coef0, degree, norms, qT, q64, scal);
       break;
     default:
-      hipLaunchKernelGGL((k_norms_q<T, KRBF>), dim3(g), dim3(NT), 0, s, Xt, ld, d, m, N, gamma,
-                         coef0, degree, norms, qT, q64, scal);
+      hipLaunchKernelGGL((k_norms_q<T, BK, TP, KRBF>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
+                         gamma, coef0, degree, norms, qT, q64, scal);
       break;
   }
   return hipGetLastError();

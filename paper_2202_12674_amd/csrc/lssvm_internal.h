@@ -11,11 +11,33 @@ namespace lssvm {
 
 enum Kern : int { KLIN = 0, KPOLY = 1, KRBF = 2 };
 
-// Points per tile edge and features per staged block, per element type.
-// The symmetric schedule needs square tiles.
+// Points per tile edge and features per staged block, per element type
+// (compile-time, like the block sizes of Sec. III-C4). The symmetric schedule
+// needs square tiles.
+#ifndef LSSVM_F32_BK
+#define LSSVM_F32_BK 32
+#endif
+#ifndef LSSVM_F64_BK
+#define LSSVM_F64_BK 16
+#endif
+// Symmetric tiles are visited in GROUP x GROUP super-tiles of the upper
+// triangle, and each of the 8 XCDs takes a contiguous run of that order, so
+// the workgroups resident on one XCD share few point panels in its L2.
+// 0 = plain column-by-column triangle order, no remap.
+#ifndef LSSVM_TILE_GROUP
+#define LSSVM_TILE_GROUP 8
+#endif
+constexpr int kNumXcd = 8;
+
+// Feature blocks in flight per workgroup in the tile kernel's register prefetch.
+#ifndef LSSVM_PREFETCH
+#define LSSVM_PREFETCH 2
+#endif
+constexpr int kPrefetch = LSSVM_PREFETCH;
+
 template <typename T> struct TileShape;
-template <> struct TileShape<float> { static constexpr int T = 128, BK = 16; };
-template <> struct TileShape<double> { static constexpr int T = 128, BK = 8; };
+template <> struct TileShape<float> { static constexpr int T = 128, BK = LSSVM_F32_BK; };
+template <> struct TileShape<double> { static constexpr int T = 128, BK = LSSVM_F64_BK; };
 
 // Slots of the small fp64 scalar area in the workspace.
 enum Scalar : int {
@@ -36,10 +58,10 @@ enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
 template <typename T>
 struct TileArgs {
-  const T* A;    // feature-major row-point panel source, A[k * lda + i]
-  const T* B;    // feature-major column-point panel source
+  const T* A;    // panel-major feature-blocked row points (see k_layout)
+  const T* B;    // panel-major feature-blocked column points
   int64_t lda, ldb;
-  int64_t nkb;   // feature blocks of BK
+  int64_t nkb;   // feature blocks of BK (even)
   const T* nA;   // squared norms of row points (RBF)
   const T* nB;   // squared norms of column points (RBF)
   const T* qA;   // q_i = k(x_i, x_m) (symmetric mode), zero beyond N
@@ -49,6 +71,7 @@ struct TileArgs {
   T gamma, coef0, qmm, invC;
   int degree;
   int64_t nTc;   // column tiles (general mode)
+  const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // partial sums, part[slot * part_ld + row]
   int64_t part_ld;
 };
@@ -57,9 +80,9 @@ template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
                          int* flags, hipStream_t s);
 template <typename T>
-hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d, int64_t m, int64_t N, int kernel,
-                          double gamma, double coef0, int degree, T* norms, T* qT, double* q64,
-                          double* scal, hipStream_t s);
+hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int64_t N,
+                          int kernel, double gamma, double coef0, int degree, T* norms, T* qT,
+                          double* q64, double* scal, hipStream_t s);
 template <typename T>
 hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s);
 template <typename T>
