@@ -230,7 +230,8 @@ __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64
 // across lanes and waves in a fixed order and written as fp64 partials,
 // one slot per tile column (rows of block I) or tile row (rows of block J).
 template <typename T, bool SYM, int KER>
-__global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles(
+    TileArgs<T> a) {
   using MF = Mfma<T>;
   using C = TileCfg<T>;
   constexpr int BM = C::BM, BK = C::BK;
@@ -376,12 +377,14 @@ __global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
     qBj[j] = SYM ? a.qB[gj[j]] : T(0);
     pBj[j] = a.pB[gj[j]];
   }
-  T rs[RB][MF::NACC];
   T cs[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) cs[j] = T(0);
+  // one row block at a time: its row sums are reduced and parked in LDS at
+  // once, which keeps few values live next to the accumulators
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
+    T rs[MF::NACC];
 #pragma unroll
     for (int v = 0; v < MF::NACC; ++v) {
       const int lr = wm * C::WM + i * MF::M + MF::row(v, lane);
@@ -402,29 +405,25 @@ __global__ __launch_bounds__(256) void k_tiles(TileArgs<T> a) {
           rsum += kv * pBj[j];
         }
       }
-      rs[i][v] = rsum;
+      rs[v] = rsum;
     }
-  }
-  // lanes that share a row differ only in the bits of cl
-#pragma unroll
-  for (int i = 0; i < RB; ++i)
+    // lanes that share a row differ only in the bits of cl
 #pragma unroll
     for (int v = 0; v < MF::NACC; ++v)
 #pragma unroll
-      for (int off = 1; off < MF::M; off <<= 1) rs[i][v] += __shfl_xor(rs[i][v], off);
+      for (int off = 1; off < MF::M; off <<= 1) rs[v] += __shfl_xor(rs[v], off);
+    if (cl == 0) {
+#pragma unroll
+      for (int v = 0; v < MF::NACC; ++v)
+        red_r[wn][wm * C::WM + i * MF::M + MF::row(v, lane)] = rs[v];
+    }
+  }
   // lanes that share a column differ only in the bits above cl
 #pragma unroll
   for (int j = 0; j < CB; ++j)
 #pragma unroll
     for (int off = MF::M; off < 64; off <<= 1) cs[j] += __shfl_xor(cs[j], off);
 
-  if (cl == 0) {
-#pragma unroll
-    for (int i = 0; i < RB; ++i)
-#pragma unroll
-      for (int v = 0; v < MF::NACC; ++v)
-        red_r[wn][wm * C::WM + i * MF::M + MF::row(v, lane)] = rs[i][v];
-  }
   if (SYM && kl == 0) {
 #pragma unroll
     for (int j = 0; j < CB; ++j) red_c[wm][wn * C::WN + j * MF::M + cl] = cs[j];
