@@ -104,7 +104,6 @@ struct TrainWs {
   double* q64;
   double* part;
   double *rhs, *x, *r, *dir, *qv;
-  T* pT;
   double *bp0, *bp1;
   double* scal;
   int* flags;
@@ -142,7 +141,6 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.r = c.take<double>(g.NP);
   w.dir = c.take<double>(g.NP);
   w.qv = c.take<double>(g.NP);
-  w.pT = c.take<T>(g.NP);
   w.bp0 = c.take<double>(g.nb + 1);
   w.bp1 = c.take<double>(g.nb + 1);
   w.scal = c.take<double>(S_COUNT);
@@ -275,7 +273,7 @@ int check_workspace(const void* ws, size_t have, size_t need) {
 
 template <typename T>
 TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                     double C, const T* p) {
+                     double C, const double* p) {
   TileArgs<T> a{};
   a.A = w.Xt;
   a.B = w.Xt;
@@ -286,8 +284,7 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.nB = w.norms;
   a.qA = w.qT;
   a.qB = w.qT;
-  a.pA = p;
-  a.pB = p;
+  a.pv = p;
   a.gamma = (T)kp.gamma;
   a.coef0 = (T)kp.coef0;
   a.degree = kp.degree;
@@ -332,7 +329,7 @@ int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t ker
 // One implicit product Q~ p into the partial-sum buffer.
 template <typename T>
 int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                    double C, int32_t kernel, const T* p, hipStream_t s) {
+                    double C, int32_t kernel, const double* p, hipStream_t s) {
   TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
   LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT), s));
   return LSSVM_OK;
@@ -340,7 +337,7 @@ int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& 
 
 template <typename T>
 int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                 double C, int32_t kernel, const T* p, hipStream_t s, MatvecTimer& tm) {
+                 double C, int32_t kernel, const double* p, hipStream_t s, MatvecTimer& tm) {
   LSSVM_HIP(tm.start(s));
   TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
   LSSVM_HIP(launch_tiles_sym<T>(a, kernel, g.nT * (g.nT + 1) / 2, s));
@@ -392,7 +389,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   // ---- setup: a1, a2, a3
   double kmm = 0.0;
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
-  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.pT, w.bp0, w.flags, s));
+  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.bp0, w.flags, s));
   LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
@@ -415,20 +412,20 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   while (!converged && it < max_iter) {
     ++it;
     const int par = (int)((it - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
-    LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.pT, s, tm));
+    LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.dir, s, tm));
     ++nmv;
     LSSVM_HIP(launch_cg_gather(w.part, g.nT, g.NP, g.N, w.dir, w.qv, w.bp0, s));
     if (it % kReplaceEvery == 0) {
-      LSSVM_HIP(launch_cg_update<T>(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.pT,
-                                    w.bp1, g.NP, s));
-      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.pT, s, tm));
+      LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
+                                 g.NP, s));
+      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.x, s, tm));
       ++nmv;
       LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, s));
     } else {
-      LSSVM_HIP(launch_cg_update<T>(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.pT,
-                                    w.bp1, g.NP, s));
+      LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
+                                 g.NP, s));
     }
-    LSSVM_HIP(launch_cg_direction<T>(w.bp1, g.nb, w.scal, par, it, w.r, w.dir, w.pT, g.NP, s));
+    LSSVM_HIP(launch_cg_direction(w.bp1, g.nb, w.scal, par, it, w.r, w.dir, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_STATUS, 4 * sizeof(double),
                              hipMemcpyDeviceToHost, s));
     LSSVM_HIP(hipStreamSynchronize(s));
@@ -467,8 +464,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     if (info->compute_true_residual) {
       double tr = 0.0;
       if (delta0 > 0.0) {
-        LSSVM_HIP(launch_cast_vec<T>(w.x, w.pT, g.NP, s));
-        LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.pT, s));
+        LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.x, s));
         LSSVM_HIP(launch_true_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.bp1, s));
         LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
         LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
@@ -498,8 +494,8 @@ int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_pa
   LSSVM_HIP(g_host.ensure());
   double kmm = 0.0;
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
-  LSSVM_HIP(launch_pad_vec<T>(p, g.N, w.pT, g.NP, s));
-  LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.pT, s));
+  LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, s));
+  LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.dir, s));
   LSSVM_HIP(launch_mv_out<T>(w.part, g.nT, g.NP, g.N, out, s));
   LSSVM_HIP(hipStreamSynchronize(s));
   return LSSVM_OK;
@@ -534,8 +530,8 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   a.nB = w.ntr;
   a.qA = nullptr;
   a.qB = nullptr;
-  a.pA = nullptr;
-  a.pB = w.alpha;
+  a.pv = nullptr;
+  a.wB = w.alpha;
   a.gamma = (T)kp.gamma;
   a.coef0 = (T)kp.coef0;
   a.degree = kp.degree;

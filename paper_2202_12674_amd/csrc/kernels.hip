@@ -262,8 +262,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ __attribute__((aligned(16))) T As1[CHUNKS * VEC];
   __shared__ __attribute__((aligned(16))) T Bs0[CHUNKS * VEC];
   __shared__ __attribute__((aligned(16))) T Bs1[CHUNKS * VEC];
-  __shared__ T red_r[WAVES_N][BM];
-  __shared__ T red_c[WAVES_M][BM];
+  __shared__ double red_r[WAVES_N][BM];
+  __shared__ double red_c[WAVES_M][BM];
 
   int64_t I, J;
   if constexpr (SYM) {
@@ -367,42 +367,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
 
   // ---- epilogue: kernel values, Q~ entries, row and column sums
+  // Kernel values and Q~ entries are formed in T; products with the vector
+  // and the sums are fp64, so an fp32 product uses the fp64 CG direction as it
+  // is instead of a rounded copy.
   const bool diag = SYM && (I == J);
   int64_t gj[CB];
-  T nBj[CB], qBj[CB], pBj[CB];
+  T nBj[CB], qBj[CB];
+  double pBj[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
     gj[j] = J * BM + wn * C::WN + j * MF::M + cl;
     nBj[j] = (KER == KRBF) ? a.nB[gj[j]] : T(0);
     qBj[j] = SYM ? a.qB[gj[j]] : T(0);
-    pBj[j] = a.pB[gj[j]];
+    if constexpr (SYM) pBj[j] = a.pv[gj[j]];
+    else pBj[j] = (double)a.wB[gj[j]];
   }
-  T cs[CB];
+  double cs[CB];
 #pragma unroll
-  for (int j = 0; j < CB; ++j) cs[j] = T(0);
+  for (int j = 0; j < CB; ++j) cs[j] = 0.0;
   // one row block at a time: its row sums are reduced and parked in LDS at
   // once, which keeps few values live next to the accumulators
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
-    T rs[MF::NACC];
+    double rs[MF::NACC];
 #pragma unroll
     for (int v = 0; v < MF::NACC; ++v) {
       const int lr = wm * C::WM + i * MF::M + MF::row(v, lane);
       const int64_t gi = I * BM + lr;
       const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
       const T qAi = SYM ? a.qA[gi] : T(0);
-      const T pAi = SYM ? a.pA[gi] : T(0);
-      T rsum = T(0);
+      const double pAi = SYM ? a.pv[gi] : 0.0;
+      double rsum = 0.0;
 #pragma unroll
       for (int j = 0; j < CB; ++j) {
         const T kv = kernel_value<KER, T>(acc[i][j][v], nAi, nBj[j], a.gamma, a.coef0, a.degree);
         if constexpr (SYM) {
           T qt = kv - qAi - qBj[j] + a.qmm;
           if (gi == gj[j]) qt += a.invC;
-          rsum += qt * pBj[j];
-          cs[j] += qt * pAi;
+          rsum += (double)qt * pBj[j];
+          cs[j] += (double)qt * pAi;
         } else {
-          rsum += kv * pBj[j];
+          rsum += (double)kv * pBj[j];
         }
       }
       rs[v] = rsum;
@@ -430,16 +435,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   __syncthreads();
   if (tid < BM) {
-    T s = T(0);
+    double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_N; ++w) s += red_r[w][tid];
-    a.part[J * a.part_ld + I * BM + tid] = (double)s;
+    a.part[J * a.part_ld + I * BM + tid] = s;
   } else if (SYM && !diag && tid < 2 * BM) {
     const int c = tid - BM;
-    T s = T(0);
+    double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
-    a.part[I * a.part_ld + J * BM + c] = (double)s;
+    a.part[I * a.part_ld + J * BM + c] = s;
   }
 }
 
@@ -447,7 +452,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 template <typename T>
 __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64_t N, int64_t NP,
                                                   double* rhs, double* x, double* r, double* dir,
-                                                  T* pT, double* bpart, int* flags) {
+                                                  double* bpart, int* flags) {
   __shared__ double sh[NT / 64];
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   const double ym = (double)y[N];
@@ -463,7 +468,6 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
     x[i] = 0.0;
     r[i] = v;
     dir[i] = v;
-    pT[i] = (T)v;
   }
   const double s = block_sum(v * v, sh);
   if (threadIdx.x == 0) bpart[blockIdx.x] = s;
@@ -503,14 +507,13 @@ __global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ pa
   if (threadIdx.x == 0) bpart[blockIdx.x] = t;
 }
 
-// x += a d and r -= a q (or, when the residual is about to be recomputed,
-// x += a d and the direction buffer receives x for that product).
-template <typename T>
+// x += a d and r -= a q (or only x += a d when the residual is about to be
+// recomputed from x).
 __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __restrict__ bp_in,
                                                    int64_t nb, double* scal, int par,
                                                    const double* __restrict__ dir,
                                                    const double* __restrict__ qv, double* x,
-                                                   double* r, T* pT, double* bp_out, int64_t NP) {
+                                                   double* r, double* bp_out, int64_t NP) {
   __shared__ double sh[NT / 64];
   const double gam = sum_partials(bp_in, nb, sh);
   const double delta = scal[S_DHIST + par];
@@ -522,11 +525,8 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double v = 0.0;
   if (i < NP) {
-    const double xi = x[i] + alpha * dir[i];
-    x[i] = xi;
-    if (x_only) {
-      pT[i] = (T)xi;
-    } else {
+    x[i] += alpha * dir[i];
+    if (!x_only) {
       const double ri = r[i] - alpha * qv[i];
       r[i] = ri;
       v = ri * ri;
@@ -575,23 +575,17 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
   if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
 }
 
-// beta = r^T r (new) / r^T r (old); d = r + beta d; the direction is also
-// written in the point dtype for the next product.
-template <typename T>
+// beta = r^T r (new) / r^T r (old); d = r + beta d.
 __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__ bp_in, int64_t nb,
                                                       double* scal, int par, int64_t iter,
                                                       const double* __restrict__ r, double* dir,
-                                                      T* pT, int64_t NP) {
+                                                      int64_t NP) {
   __shared__ double sh[NT / 64];
   const double dnew = sum_partials(bp_in, nb, sh);
   const double dold = scal[S_DHIST + par];
   const double beta = dnew / dold;
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i < NP) {
-    const double di = r[i] + beta * dir[i];
-    dir[i] = di;
-    pT[i] = (T)di;
-  }
+  if (i < NP) dir[i] = r[i] + beta * dir[i];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_DHIST + (par ^ 1)] = dnew;
     scal[S_STATUS + 0] = dnew;
@@ -670,10 +664,10 @@ __global__ __launch_bounds__(256) void k_predict_finish(const double* __restrict
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_cast_vec(const double* __restrict__ src,
-                                                  T* __restrict__ dst, int64_t len) {
+__global__ __launch_bounds__(256) void k_pad_to_f64(const T* __restrict__ src, int64_t len,
+                                                    double* __restrict__ dst, int64_t len_pad) {
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i < len) dst[i] = (T)src[i];
+  if (i < len_pad) dst[i] = i < len ? (double)src[i] : 0.0;
 }
 
 __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t nb, double* scal,
@@ -747,9 +741,9 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
-                           double* dir, T* pT, double* bpart, int* flags, hipStream_t s) {
+                           double* dir, double* bpart, int* flags, hipStream_t s) {
   hipLaunchKernelGGL(k_rhs_init<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
-                     dir, pT, bpart, flags);
+                     dir, bpart, flags);
   return hipGetLastError();
 }
 
@@ -765,12 +759,11 @@ hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int6
   return hipGetLastError();
 }
 
-template <typename T>
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
-                            const double* dir, const double* qv, double* x, double* r, T* pT,
+                            const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_update<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, x_only, bp_in, nb,
-                     scal, par, dir, qv, x, r, pT, bp_out, NP);
+  hipLaunchKernelGGL(k_cg_update, dim3(blocks_for(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
+                     par, dir, qv, x, r, bp_out, NP);
   return hipGetLastError();
 }
 
@@ -788,12 +781,11 @@ hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, 
   return hipGetLastError();
 }
 
-template <typename T>
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
-                               int64_t iter, const double* r, double* dir, T* pT, int64_t NP,
+                               int64_t iter, const double* r, double* dir, int64_t NP,
                                hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_direction<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, bp_in, nb, scal,
-                     par, iter, r, dir, pT, NP);
+  hipLaunchKernelGGL(k_cg_direction, dim3(blocks_for(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
+                     iter, r, dir, NP);
   return hipGetLastError();
 }
 
@@ -834,8 +826,10 @@ hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld,
 }
 
 template <typename T>
-hipError_t launch_cast_vec(const double* src, T* dst, int64_t len, hipStream_t s) {
-  hipLaunchKernelGGL(k_cast_vec<T>, dim3(blocks_for(len)), dim3(NT), 0, s, src, dst, len);
+hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len_pad,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(k_pad_to_f64<T>, dim3(blocks_for(len_pad)), dim3(NT), 0, s, src, len, dst,
+                     len_pad);
   return hipGetLastError();
 }
 
@@ -854,12 +848,7 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
   template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
   template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
   template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
-                                         double*, T*, double*, int*, hipStream_t);                \
-  template hipError_t launch_cg_update<T>(int, const double*, int64_t, double*, int,              \
-                                          const double*, const double*, double*, double*, T*,     \
-                                          double*, int64_t, hipStream_t);                         \
-  template hipError_t launch_cg_direction<T>(const double*, int64_t, double*, int, int64_t,       \
-                                             const double*, double*, T*, int64_t, hipStream_t);   \
+                                         double*, double*, int*, hipStream_t);                    \
   template hipError_t launch_bias<T>(const double*, const double*, int64_t, const T*, double*,    \
                                      double, T*, hipStream_t);                                    \
   template hipError_t launch_single_point<T>(const T*, T*, double*, int*, hipStream_t);           \
@@ -868,7 +857,7 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
                                        hipStream_t);                                              \
   template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
                                                T*, int32_t*, hipStream_t);                        \
-  template hipError_t launch_cast_vec<T>(const double*, T*, int64_t, hipStream_t);
+  template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, hipStream_t);
 
 LSSVM_INSTANTIATE(float)
 LSSVM_INSTANTIATE(double)

@@ -66,8 +66,8 @@ struct TileArgs {
   const T* nB;   // squared norms of column points (RBF)
   const T* qA;   // q_i = k(x_i, x_m) (symmetric mode), zero beyond N
   const T* qB;
-  const T* pA;   // vector multiplied into column sums (symmetric mode)
-  const T* pB;   // vector multiplied into row sums (p, or alpha in predict)
+  const double* pv;  // symmetric mode: the vector multiplied (fp64), zero beyond N
+  const T* wB;       // general mode: per-column weights (alpha)
   T gamma, coef0, qmm, invC;
   int degree;
   int64_t nTc;   // column tiles (general mode)
@@ -89,19 +89,17 @@ template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
-                           double* dir, T* pT, double* bpart, int* flags, hipStream_t s);
+                           double* dir, double* bpart, int* flags, hipStream_t s);
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, hipStream_t s);
 hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
                             const double* dir, double* qv, double* bpart, hipStream_t s);
-template <typename T>
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
-                            const double* dir, const double* qv, double* x, double* r, T* pT,
+                            const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s);
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, hipStream_t s);
-template <typename T>
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
-                               int64_t iter, const double* r, double* dir, T* pT, int64_t NP,
+                               int64_t iter, const double* r, double* dir, int64_t NP,
                                hipStream_t s);
 template <typename T>
 hipError_t launch_bias(const double* x, const double* q64, int64_t N, const T* y, double* scal,
@@ -117,7 +115,8 @@ template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
                                  double b, T* scores, int32_t* labels, hipStream_t s);
 template <typename T>
-hipError_t launch_cast_vec(const double* src, T* dst, int64_t len, hipStream_t s);
+hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len_pad,
+                             hipStream_t s);
 hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int slot,
                              hipStream_t s);
 hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
