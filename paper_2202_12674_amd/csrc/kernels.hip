@@ -254,8 +254,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   typedef __attribute__((address_space(3))) void* lptr_t;
 
   // LDS: per stage and panel, BM rows of 128 bytes; chunk c of point p sits at
-  // physical chunk p * 8 + (c ^ (p & 7)), so both the lane-linear direct
-  // loads and the 16-byte operand reads hit distinct banks.
+  // physical chunk p * 8 + (c ^ ((p >> 1) & 7)). A 16-byte read serves 16
+  // lanes (16 consecutive points, one logical chunk) per cycle: rows of even
+  // and odd p fall in opposite bank halves, and (p >> 1) & 7 spreads each
+  // half over its 8 four-bank groups, so the reads are conflict-free; the
+  // lane-linear direct loads are conflict-free by construction.
   // one array per stage and panel: with fixed names the compiler can tell the
   // stage being filled from the stage being read and need not wait in between
   __shared__ __attribute__((aligned(16))) T As0[CHUNKS * VEC];
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
   for (int u = 0; u < LOADS; ++u) {
     const int P = (u * 4 + wave) * 64 + lane;
-    const int p = P / CPR, c = (P % CPR) ^ (p & 7);
+    const int p = P / CPR, c = (P % CPR) ^ ((p >> 1) & 7);
     goff[u] = (p * CPR + c) * VEC;
   }
   auto dload = [&](int64_t kb, T (&sa)[CHUNKS * VEC], T (&sb)[CHUNKS * VEC]) {
@@ -328,7 +331,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
       for (int q = 0; q < CPG; ++q)
         av[i][q] = *reinterpret_cast<const vec_t*>(
-            &sa[(p * CPR + ((kl * CPG + q) ^ (p & 7))) * VEC]);
+            &sa[(p * CPR + ((kl * CPG + q) ^ ((p >> 1) & 7))) * VEC]);
     }
 #pragma unroll
     for (int j = 0; j < CB; ++j) {
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
       for (int q = 0; q < CPG; ++q)
         bv[j][q] = *reinterpret_cast<const vec_t*>(
-            &sb[(p * CPR + ((kl * CPG + q) ^ (p & 7))) * VEC]);
+            &sb[(p * CPR + ((kl * CPG + q) ^ ((p >> 1) & 7))) * VEC]);
     }
 #pragma unroll
     for (int kk = 0; kk < FPG; ++kk)
@@ -387,11 +390,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (int j = 0; j < CB; ++j) cs[j] = 0.0;
   // one row block at a time: its row sums are reduced and parked in LDS at
   // once, which keeps few values live next to the accumulators
+  constexpr int VH = MF::NACC > 8 ? 8 : MF::NACC;   // accumulator elements per pass
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
-    double rs[MF::NACC];
 #pragma unroll
-    for (int v = 0; v < MF::NACC; ++v) {
+  for (int v0 = 0; v0 < MF::NACC; v0 += VH) {
+    double rs[VH];
+#pragma unroll
+    for (int vv = 0; vv < VH; ++vv) {
+      const int v = v0 + vv;
       const int lr = wm * C::WM + i * MF::M + MF::row(v, lane);
       const int64_t gi = I * BM + lr;
       const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
@@ -410,18 +417,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
           rsum += (double)kv * pBj[j];
         }
       }
-      rs[v] = rsum;
+      rs[vv] = rsum;
     }
     // lanes that share a row differ only in the bits of cl
 #pragma unroll
-    for (int v = 0; v < MF::NACC; ++v)
+    for (int vv = 0; vv < VH; ++vv)
 #pragma unroll
-      for (int off = 1; off < MF::M; off <<= 1) rs[v] += __shfl_xor(rs[v], off);
+      for (int off = 1; off < MF::M; off <<= 1) rs[vv] += __shfl_xor(rs[vv], off);
     if (cl == 0) {
 #pragma unroll
-      for (int v = 0; v < MF::NACC; ++v)
-        red_r[wn][wm * C::WM + i * MF::M + MF::row(v, lane)] = rs[v];
+      for (int vv = 0; vv < VH; ++vv)
+        red_r[wn][wm * C::WM + i * MF::M + MF::row(v0 + vv, lane)] = rs[vv];
     }
+  }
   }
   // lanes that share a column differ only in the bits above cl
 #pragma unroll
