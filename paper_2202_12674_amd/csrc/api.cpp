@@ -108,6 +108,7 @@ struct TrainWs {
   double* scal;
   int* flags;
   uint32_t* order;
+  double* hist;
   size_t bytes;
 };
 
@@ -146,6 +147,7 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.scal = c.take<double>(S_COUNT);
   w.flags = c.take<int>(F_COUNT);
   w.order = c.take<uint32_t>(LSSVM_TILE_GROUP > 0 ? tri_count(g.nT) : 0);
+  w.hist = c.take<double>(g.NP + 1);   // r^T r after each iteration (at most N of them)
   w.bytes = c.off;
   return w;
 }
@@ -195,9 +197,13 @@ struct HostScratch {
 thread_local HostScratch g_host;
 
 // HIP events around each implicit product, recorded on the launch stream.
+// Pairs carry the CG iteration they belong to, so products that ran after
+// the stop (and returned at once) are left out.
 struct MatvecTimer {
+  static constexpr int kPairs = 2 * 64;   // up to two products per queued iteration
   bool on = false;
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t ev[2 * kPairs] = {};
+  int64_t tag[kPairs] = {};
   int used = 0;          // event pairs recorded since the last harvest
   double total_ms = 0.0;
   int64_t count = 0;
@@ -214,16 +220,21 @@ struct MatvecTimer {
     for (auto& e : ev)
       if (e) (void)hipEventDestroy(e);
   }
-  hipError_t start(hipStream_t s) { return on ? hipEventRecord(ev[2 * used], s) : hipSuccess; }
+  hipError_t start(hipStream_t s, int64_t iter) {
+    if (!on) return hipSuccess;
+    tag[used] = iter;
+    return hipEventRecord(ev[2 * used], s);
+  }
   hipError_t stop(hipStream_t s) {
     if (!on) return hipSuccess;
     hipError_t r = hipEventRecord(ev[2 * used + 1], s);
     ++used;
     return r;
   }
-  // After the stream has been synchronised: add the recorded pairs.
-  hipError_t harvest() {
+  // After the stream has been synchronised: add the pairs of iterations <= last.
+  hipError_t harvest(int64_t last) {
     for (int i = 0; i < used; ++i) {
+      if (tag[i] > last) continue;
       float ms = 0.f;
       hipError_t r = hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]);
       if (r != hipSuccess) return r;
@@ -337,9 +348,11 @@ int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& 
 
 template <typename T>
 int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                 double C, int32_t kernel, const double* p, hipStream_t s, MatvecTimer& tm) {
-  LSSVM_HIP(tm.start(s));
+                 double C, int32_t kernel, const double* p, hipStream_t s, MatvecTimer& tm,
+                 int64_t iter) {
+  LSSVM_HIP(tm.start(s, iter));
   TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
+  a.status = w.scal + S_STATUS;   // skip the launch once CG has stopped
   LSSVM_HIP(launch_tiles_sym<T>(a, kernel, g.nT * (g.nT + 1) / 2, s));
   LSSVM_HIP(tm.stop(s));
   return LSSVM_OK;
@@ -390,7 +403,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   double kmm = 0.0;
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
   LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.bp0, w.flags, s));
-  LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, s));
+  LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
@@ -402,48 +415,55 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   LSSVM_HIP(tm.init(info && info->time_matvec));
 
   // ---- a4 + a5: conjugate gradients
+  // Iterations are enqueued in batches (1, 2, 4, ... up to 32) and the status
+  // is read once per batch; kernels queued after the stop return at once, so
+  // the iterate is the one of the stopping iteration.
   const auto t1 = clock_t_::now();
   if (max_iter <= 0) max_iter = g.N;
-  int64_t it = 0, nmv = 0;
-  bool converged = delta0 == 0.0;  // all labels equal: alpha~ = 0 solves the system
+  int64_t queued = 0, it = 0;
+  bool done = delta0 == 0.0;  // all labels equal: alpha~ = 0 solves the system
+  bool broke = false;
   double delta = delta0;
   int status = LSSVM_OK;
-  const double stop = eps * eps * delta0;
-  while (!converged && it < max_iter) {
-    ++it;
-    const int par = (int)((it - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
-    LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.dir, s, tm));
-    ++nmv;
-    LSSVM_HIP(launch_cg_gather(w.part, g.nT, g.NP, g.N, w.dir, w.qv, w.bp0, s));
-    if (it % kReplaceEvery == 0) {
-      LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
-                                 g.NP, s));
-      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.x, s, tm));
-      ++nmv;
-      LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, s));
-    } else {
-      LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
-                                 g.NP, s));
+  int64_t batch = 1;
+  double* st = g_host.p;
+  while (!done && queued < max_iter) {
+    const int64_t nq = std::min<int64_t>(batch, max_iter - queued);
+    for (int64_t b = 0; b < nq; ++b) {
+      const int64_t k = ++queued;
+      const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
+      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.dir, s, tm, k));
+      LSSVM_HIP(launch_cg_gather(w.part, g.nT, g.NP, g.N, w.dir, w.qv, w.bp0, w.scal, s));
+      if (k % kReplaceEvery == 0) {
+        LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
+                                   g.NP, s));
+        LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.x, s, tm, k));
+        LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+      } else {
+        LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
+                                   g.NP, s));
+      }
+      LSSVM_HIP(launch_cg_direction(w.bp1, g.nb, w.scal, par, k, w.r, w.dir, g.NP, w.hist,
+                                    g.NP + 1, s));
     }
-    LSSVM_HIP(launch_cg_direction(w.bp1, g.nb, w.scal, par, it, w.r, w.dir, g.NP, s));
-    LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_STATUS, 4 * sizeof(double),
+    LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
     LSSVM_HIP(hipStreamSynchronize(s));
-    LSSVM_HIP(tm.harvest());
-    const double dnew = g_host.p[0], curv = g_host.p[1], step = g_host.p[2];
-    if (!(curv > 0.0) || !std::isfinite(curv) || !std::isfinite(step) || !std::isfinite(dnew)) {
+    it = (int64_t)st[ST_ITER];
+    done = st[ST_DONE] != 0.0;
+    broke = st[ST_BREAK] != 0.0;
+    LSSVM_HIP(tm.harvest(done ? it : queued));
+    if (broke) {
+      it += 1;   // the update of the next iteration found the curvature
       status = fail(LSSVM_EBREAKDOWN, "CG breakdown at iteration %lld (d^T Q d = %g)",
-                    (long long)it, curv);
+                    (long long)it, st[ST_CURV]);
       break;
     }
-    delta = dnew;
-    if (info && info->residual_history && it <= info->history_capacity)
-      info->residual_history[it - 1] = delta / delta0;
-    if (delta <= stop) {
-      converged = true;
-      break;
-    }
+    delta = st[ST_DELTA];
+    batch = std::min<int64_t>(2 * batch, 32);
   }
+  const bool converged = done && !broke;
+  const int64_t nmv = it + it / kReplaceEvery;
   const double t_cg = ms_since(t1);
   if (status == LSSVM_OK && !converged) {
     status = LSSVM_NOT_CONVERGED;
@@ -451,6 +471,15 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
          (long long)it, std::sqrt(delta / delta0));
   }
   if (status < 0) return status;
+  if (info && info->residual_history && it > 0) {
+    const int64_t nh = std::min(std::min(it, info->history_capacity), g.NP + 1);
+    if (nh > 0) {
+      LSSVM_HIP(hipMemcpyAsync(info->residual_history, w.hist, nh * sizeof(double),
+                               hipMemcpyDeviceToHost, s));
+      LSSVM_HIP(hipStreamSynchronize(s));
+      for (int64_t k = 0; k < nh; ++k) info->residual_history[k] /= delta0;
+    }
+  }
 
   // ---- a6: alpha_m and b
   LSSVM_HIP(launch_bias<T>(w.x, w.q64, g.N, y, w.scal, 1.0 / C, alpha_out, s));

@@ -268,6 +268,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ double red_r[WAVES_N][BM];
   __shared__ double red_c[WAVES_M][BM];
 
+  if constexpr (SYM) {
+    if (a.status && a.status[ST_DONE] != 0.0) return;   // CG already stopped
+  }
   int64_t I, J;
   if constexpr (SYM) {
     if (a.order) {
@@ -482,16 +485,20 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
 }
 
 __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int64_t nb,
-                                                       double* scal) {
+                                                       double* scal, double eps2) {
   __shared__ double sh[NT / 64];
   const double s = sum_partials(bpart, nb, sh);
   if (threadIdx.x == 0) {
     scal[S_DELTA0] = s;
     scal[S_DHIST + 0] = s;
-    scal[S_STATUS + 0] = s;
-    scal[S_STATUS + 1] = 0.0;
-    scal[S_STATUS + 2] = 0.0;
-    scal[S_STATUS + 3] = 0.0;
+    double* st = scal + S_STATUS;
+    st[ST_DELTA] = s;
+    st[ST_CURV] = 0.0;
+    st[ST_STEP] = 0.0;
+    st[ST_ITER] = 0.0;
+    st[ST_DONE] = s == 0.0 ? 1.0 : 0.0;   // all labels equal: alpha~ = 0 solves it
+    st[ST_BREAK] = 0.0;
+    st[ST_STOP] = eps2 * s;
   }
 }
 
@@ -500,8 +507,9 @@ __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int6
 __global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ part, int64_t nslots,
                                                    int64_t NP, int64_t N,
                                                    const double* __restrict__ dir, double* qv,
-                                                   double* bpart) {
+                                                   double* bpart, const double* scal) {
   __shared__ double sh[NT / 64];
+  if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double prod = 0.0;
   if (i < NP) {
@@ -523,12 +531,19 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
                                                    const double* __restrict__ qv, double* x,
                                                    double* r, double* bp_out, int64_t NP) {
   __shared__ double sh[NT / 64];
+  if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const double gam = sum_partials(bp_in, nb, sh);
   const double delta = scal[S_DHIST + par];
   const double alpha = delta / gam;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_ALPHA] = alpha;
     scal[S_GAMMA] = gam;
+    if (!(gam > 0.0) || !__builtin_isfinite(alpha)) {   // curvature breakdown
+      scal[S_STATUS + ST_CURV] = gam;
+      scal[S_STATUS + ST_STEP] = alpha;
+      scal[S_STATUS + ST_BREAK] = 1.0;
+      scal[S_STATUS + ST_DONE] = 1.0;
+    }
   }
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double v = 0.0;
@@ -550,8 +565,9 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
 __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part,
                                                      int64_t nslots, int64_t NP, int64_t N,
                                                      const double* __restrict__ rhs, double* r,
-                                                     double* bp_out) {
+                                                     double* bp_out, const double* scal) {
   __shared__ double sh[NT / 64];
+  if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double v = 0.0;
   if (i < NP) {
@@ -583,12 +599,16 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
   if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
 }
 
-// beta = r^T r (new) / r^T r (old); d = r + beta d.
+// beta = r^T r (new) / r^T r (old); d = r + beta d. Block 0 records the
+// iteration in the status (and the history) and raises done once
+// r^T r <= eps^2 r0^T r0.
 __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__ bp_in, int64_t nb,
                                                       double* scal, int par, int64_t iter,
                                                       const double* __restrict__ r, double* dir,
-                                                      int64_t NP) {
+                                                      int64_t NP, double* hist, int64_t hist_cap) {
   __shared__ double sh[NT / 64];
+  double* st = scal + S_STATUS;
+  if (st[ST_DONE] != 0.0) return;
   const double dnew = sum_partials(bp_in, nb, sh);
   const double dold = scal[S_DHIST + par];
   const double beta = dnew / dold;
@@ -596,10 +616,12 @@ __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__
   if (i < NP) dir[i] = r[i] + beta * dir[i];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_DHIST + (par ^ 1)] = dnew;
-    scal[S_STATUS + 0] = dnew;
-    scal[S_STATUS + 1] = scal[S_GAMMA];
-    scal[S_STATUS + 2] = scal[S_ALPHA];
-    scal[S_STATUS + 3] = (double)iter;
+    st[ST_DELTA] = dnew;
+    st[ST_CURV] = scal[S_GAMMA];
+    st[ST_STEP] = scal[S_ALPHA];
+    st[ST_ITER] = (double)iter;
+    if (iter <= hist_cap) hist[iter - 1] = dnew;
+    if (dnew <= st[ST_STOP]) st[ST_DONE] = 1.0;
   }
 }
 
@@ -755,15 +777,17 @@ hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, doubl
   return hipGetLastError();
 }
 
-hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, hipStream_t s) {
-  hipLaunchKernelGGL(k_finish_delta0, dim3(1), dim3(NT), 0, s, bpart, nb, scal);
+hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(k_finish_delta0, dim3(1), dim3(NT), 0, s, bpart, nb, scal, eps2);
   return hipGetLastError();
 }
 
 hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                            const double* dir, double* qv, double* bpart, hipStream_t s) {
+                            const double* dir, double* qv, double* bpart, const double* scal,
+                            hipStream_t s) {
   hipLaunchKernelGGL(k_cg_gather, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N, dir,
-                     qv, bpart);
+                     qv, bpart, scal);
   return hipGetLastError();
 }
 
@@ -776,9 +800,10 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 }
 
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, hipStream_t s) {
+                              const double* rhs, double* r, double* bp_out, const double* scal,
+                              hipStream_t s) {
   hipLaunchKernelGGL(k_cg_residual, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N,
-                     rhs, r, bp_out);
+                     rhs, r, bp_out, scal);
   return hipGetLastError();
 }
 
@@ -791,9 +816,9 @@ hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, 
 
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
-                               hipStream_t s) {
+                               double* hist, int64_t hist_cap, hipStream_t s) {
   hipLaunchKernelGGL(k_cg_direction, dim3(blocks_for(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
-                     iter, r, dir, NP);
+                     iter, r, dir, NP, hist, hist_cap);
   return hipGetLastError();
 }
 

@@ -48,12 +48,14 @@ enum Scalar : int {
   S_ALPHA = 5,   // CG step length of the last update
   S_GAMMA = 6,   // curvature d^T Q~ d of the last update
   S_TRUE = 7,    // ||rhs - Q~ x||^2 (final report)
-  S_STATUS = 8,  // 4 doubles copied to the host each iteration:
-                 // [0] r^T r, [1] curvature, [2] step length, [3] iteration tag
+  S_STATUS = 8,  // 8 doubles read by the host after each batch of iterations:
+                 // [0] r^T r of the last iteration run, [1] its curvature,
+                 // [2] its step length, [3] its number, [4] done (converged or
+                 // broken down), [5] breakdown, [6] stop threshold eps^2 r0^T r0
   S_COUNT = 16
 };
-
-// Flags raised by kernels (int32 each).
+enum StatusField : int { ST_DELTA = 0, ST_CURV = 1, ST_STEP = 2, ST_ITER = 3, ST_DONE = 4,
+                         ST_BREAK = 5, ST_STOP = 6, ST_COUNT = 8 };// Flags raised by kernels (int32 each).
 enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
 template <typename T>
@@ -73,6 +75,7 @@ struct TileArgs {
   int64_t nTc;   // column tiles (general mode)
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // partial sums, part[slot * part_ld + row]
+  const double* status;  // symmetric mode: CG status (skip the launch once done) or null
   int64_t part_ld;
 };
 
@@ -90,17 +93,22 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
                            double* dir, double* bpart, int* flags, hipStream_t s);
-hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, hipStream_t s);
+// CG kernels: once the status says done, every later kernel of the queue
+// returns at once, so the host may enqueue iterations ahead of the test.
+hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
+                                hipStream_t s);
 hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                            const double* dir, double* qv, double* bpart, hipStream_t s);
+                            const double* dir, double* qv, double* bpart, const double* scal,
+                            hipStream_t s);
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s);
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, hipStream_t s);
+                              const double* rhs, double* r, double* bp_out, const double* scal,
+                              hipStream_t s);
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
-                               hipStream_t s);
+                               double* hist, int64_t hist_cap, hipStream_t s);
 template <typename T>
 hipError_t launch_bias(const double* x, const double* q64, int64_t N, const T* y, double* scal,
                        double invC, T* alpha_out, hipStream_t s);

@@ -384,3 +384,23 @@ def test_train_deterministic(torch_dev):
     b = P.train(Xd, yd, C=1.0, eps=1e-5, **kw_of(cfg))
     assert a.iterations == b.iterations and a.b == b.b
     assert torch.equal(a.alpha, b.alpha)
+
+
+def test_train_max_iter_beyond_n_and_long_history(torch_dev):
+    """max_iter far above N and a history buffer longer than the run: CG stops at eps,
+    the history holds exactly the iterations run, matching the oracle's recurrence."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("linear", "f64", 40, 6)
+    X, y, _, _ = data_of(cfg)
+    r = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=1.0, eps=1e-12,
+                max_iter=100_000, history=5000)
+    Qt, _, _ = O.reduced_matrix(X, O.KernelSpec("linear"), 1.0)
+    rhs = O.reduced_rhs(y)
+    ref = O.solve_cg(lambda v: Qt @ v, rhs, 1e-12, max_iter=100_000)
+    assert r.converged and r.iterations <= 39 + 5
+    assert abs(r.iterations - ref.iterations) <= 2
+    assert len(r.history) == r.iterations
+    k = min(len(r.history), len(ref.history), 10)
+    d0 = float(rhs @ rhs)
+    assert np.allclose(r.history[:k], np.array(ref.history[:k]) / d0, rtol=1e-8, atol=1e-15)
