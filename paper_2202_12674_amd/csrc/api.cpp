@@ -158,6 +158,8 @@ struct PredictWs {
   T *Xte, *nte;
   double* part;
   int* flags;
+  double* lin_part;  // linear kernel: partial sums of w over point chunks
+  double* lin_w;     // linear kernel: w = sum_i alpha_i x_i
   int64_t ld_te, nTc, nTr;
   size_t bytes;
 };
@@ -176,6 +178,8 @@ PredictWs<T> carve_predict(const Geometry& g, int64_t n_test, void* base) {
   w.nte = c.take<T>(w.ld_te);
   w.part = c.take<double>(w.nTc * w.ld_te);
   w.flags = c.take<int>(F_COUNT);
+  w.lin_part = c.take<double>(linear_predict_part_elems(g.n, g.d));
+  w.lin_w = c.take<double>(g.d);
   w.bytes = c.off;
   return w;
 }
@@ -540,6 +544,16 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   w = carve_predict<T>(g, n_test, workspace);
   LSSVM_HIP(g_host.ensure());
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
+  if (kernel == LSSVM_LINEAR) {  // Eq. (15): w = sum_i alpha_i x_i, f(x) = <w, x> + b
+    LSSVM_HIP(launch_linear_predict<T>(Xtr, alpha, n, d, Xte, n_test, b, w.lin_part, w.lin_w,
+                                       scores, labels, w.flags, s));
+    LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+                             s));
+    LSSVM_HIP(hipStreamSynchronize(s));
+    if (g_host.flags[F_NONFINITE])
+      return fail(LSSVM_ENONFINITE, "X_train or X_test holds a NaN or an infinity");
+    return LSSVM_OK;
+  }
   LSSVM_HIP(launch_layout<T>(Xtr, n, d, w.Xtr, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_layout<T>(Xte, n_test, d, w.Xte, w.ld_te, g.d_pad, w.flags, s));
   if (kernel == LSSVM_RBF) {  // squared norms are only read by the radial kernel

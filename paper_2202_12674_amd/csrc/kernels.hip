@@ -660,6 +660,74 @@ __global__ void k_single_point(const T* __restrict__ y, T* __restrict__ alpha_ou
   }
 }
 
+// --------------------------------------------- a7 linear-kernel shortcut ----
+// For the linear kernel Phi is the identity, so w = sum_i alpha_i x_i (Eq. (15))
+// and f(x) = <w, x> + b: O((n + n_test) d) instead of a tile contraction.
+// Partial sums of w over chunks of kLinRows points (coalesced over features),
+// then a fixed-order sum of the chunks.
+constexpr int kLinRows = 64;
+constexpr int64_t kLinMaxChunks = 32768;   // stays inside the 65535 grid limit in y
+inline int64_t lin_rows(int64_t n) {
+  const int64_t r = (n + kLinMaxChunks - 1) / kLinMaxChunks;
+  return r > kLinRows ? r : kLinRows;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_linear_w_part(const T* __restrict__ X,
+                                                       const T* __restrict__ alpha, int64_t n,
+                                                       int64_t d, int64_t rows,
+                                                       double* __restrict__ part,
+                                                       int* __restrict__ flags) {
+  const int64_t k = (int64_t)blockIdx.x * NT + threadIdx.x;
+  const int64_t i0 = (int64_t)blockIdx.y * rows;
+  if (k >= d) return;
+  double acc = 0.0;
+  bool bad = false;
+  const int64_t i1 = i0 + rows < n ? i0 + rows : n;
+  for (int64_t i = i0; i < i1; ++i) {
+    const T xv = X[i * d + k];
+    bad |= !__builtin_isfinite(xv);
+    acc += (double)alpha[i] * (double)xv;
+  }
+  part[(int64_t)blockIdx.y * d + k] = acc;
+  if (bad) flags[F_NONFINITE] = 1;
+}
+
+__global__ __launch_bounds__(256) void k_linear_w_sum(const double* __restrict__ part,
+                                                      int64_t nchunks, int64_t d,
+                                                      double* __restrict__ w) {
+  const int64_t k = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (k >= d) return;
+  double s = 0.0;
+  for (int64_t c = 0; c < nchunks; ++c) s += part[c * d + k];
+  w[k] = s;
+}
+
+// One block per test point: f = <w, x> + b (fp64), label +1 iff f > 0.
+template <typename T>
+__global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte, int64_t n_test,
+                                                       int64_t d, const double* __restrict__ w,
+                                                       double b, T* __restrict__ scores,
+                                                       int32_t* __restrict__ labels,
+                                                       int* __restrict__ flags) {
+  __shared__ double sh[NT / 64];
+  const int64_t t = blockIdx.x;
+  const T* x = Xte + t * d;
+  double acc = 0.0;
+  bool bad = false;
+  for (int64_t k = threadIdx.x; k < d; k += NT) {
+    const T xv = x[k];
+    bad |= !__builtin_isfinite(xv);
+    acc += (double)xv * w[k];
+  }
+  if (bad) flags[F_NONFINITE] = 1;
+  const double f = block_sum(acc, sh) + b;
+  if (threadIdx.x == 0) {
+    scores[t] = (T)f;
+    if (labels) labels[t] = f > 0.0 ? 1 : -1;
+  }
+}
+
 // ---------------------------------------------------------- misc vectors ----
 template <typename T>
 __global__ __launch_bounds__(256) void k_pad_vec(const T* __restrict__ src, int64_t len,
@@ -872,6 +940,30 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
   return hipGetLastError();
 }
 
+template <typename T>
+hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_t d, const T* Xte,
+                                 int64_t n_test, double b, double* part, double* w, T* scores,
+                                 int32_t* labels, int* flags, hipStream_t s) {
+  const int64_t rows = lin_rows(n);
+  const int64_t nchunks = (n + rows - 1) / rows;
+  const unsigned gx = (unsigned)((d + NT - 1) / NT);
+  hipLaunchKernelGGL(k_linear_w_part<T>, dim3(gx, (unsigned)nchunks), dim3(NT), 0, s, Xtr, alpha,
+                     n, d, rows, part, flags);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_linear_w_sum, dim3(gx), dim3(NT), 0, s, part, nchunks, d, w);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_linear_scores<T>, dim3((unsigned)n_test), dim3(NT), 0, s, Xte, n_test, d,
+                     w, b, scores, labels, flags);
+  return hipGetLastError();
+}
+
+int64_t linear_predict_part_elems(int64_t n, int64_t d) {
+  const int64_t rows = lin_rows(n);
+  return (n + rows - 1) / rows * d;
+}
+
 #define LSSVM_INSTANTIATE(T)                                                                      \
   template hipError_t launch_layout<T>(const T*, int64_t, int64_t, T*, int64_t, int64_t, int*,    \
                                        hipStream_t);                                              \
@@ -890,7 +982,10 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
                                        hipStream_t);                                              \
   template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
                                                T*, int32_t*, hipStream_t);                        \
-  template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, hipStream_t);
+  template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, hipStream_t);   \
+  template hipError_t launch_linear_predict<T>(const T*, const T*, int64_t, int64_t, const T*,    \
+                                               int64_t, double, double*, double*, T*, int32_t*,   \
+                                               int*, hipStream_t);
 
 LSSVM_INSTANTIATE(float)
 LSSVM_INSTANTIATE(double)

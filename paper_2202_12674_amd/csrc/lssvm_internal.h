@@ -130,4 +130,12 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
 hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                                 const double* rhs, double* bp_out, hipStream_t s);
 
+// Linear-kernel decision values through w = sum_i alpha_i x_i (Eq. (15)).
+// part: linear_predict_part_elems(n, d) doubles; w: d doubles.
+template <typename T>
+hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_t d, const T* Xte,
+                                 int64_t n_test, double b, double* part, double* w, T* scores,
+                                 int32_t* labels, int* flags, hipStream_t s);
+int64_t linear_predict_part_elems(int64_t n, int64_t d);
+
 }  // namespace lssvm

@@ -404,3 +404,22 @@ def test_train_max_iter_beyond_n_and_long_history(torch_dev):
     k = min(len(r.history), len(ref.history), 10)
     d0 = float(rhs @ rhs)
     assert np.allclose(r.history[:k], np.array(ref.history[:k]) / d0, rtol=1e-8, atol=1e-15)
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_predict_linear_shortcut_large(torch_dev, dtype):
+    """Linear decision values through w = sum alpha_i x_i against the oracle's kernel
+    rows at 4096 training x 1024 test points."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("linear", dtype, 4096, 1024)
+    X, y, Xte, _ = data_of(cfg)
+    alpha = np.random.default_rng(4).standard_normal(cfg.n).astype(cfg.np_dtype)
+    b = -0.25
+    f_ref, _ = O.predict(X, alpha, b, Xte, O.KernelSpec("linear"))
+    scores, labels = P.predict(to_dev(torch, dev, X), to_dev(torch, dev, alpha), b,
+                               to_dev(torch, dev, Xte))
+    tol = TOL_MV[dtype]
+    assert rel_err(scores.cpu().numpy(), f_ref) <= tol * 10
+    bad, _ = labels_match(labels.cpu().numpy(), f_ref, tol * 10)
+    assert bad == 0
