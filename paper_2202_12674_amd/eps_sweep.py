@@ -1,0 +1,124 @@
+"""Runtime, CG iterations and accuracy against the relative-residual target eps.
+
+The paper studies how eps drives the CG iteration count, the runtime and the
+accuracy (Sec. IV-F), and chooses eps for its comparisons by a protocol
+(Sec. IV-B): start at 0.1 and divide by 10 until the training accuracy
+exceeds 97%; if that never happens, take the first eps whose accuracy agrees
+with the next smaller eps in the first three digits.
+
+This harness trains once per eps on the GPU (lssvm_train), predicts the
+training points and held-out points (lssvm_predict) and reports one JSON
+line per eps plus a summary line with the eps the protocol picks.
+
+    python -m paper_2202_12674_amd.eps_sweep [--n 32768 --d 4096 --kernel linear --dtype f64]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+DEFAULT_EPS = [10.0 ** (-k) for k in range(1, 16)]
+
+
+def tune_eps(rows, target: float = 0.97):
+    """The eps-selection protocol of Sec. IV-B applied to sweep rows ordered by
+    decreasing eps: the first eps whose training accuracy exceeds `target`;
+    otherwise the first eps whose accuracy equals the next one in three digits;
+    otherwise the smallest eps."""
+    for r in rows:
+        if r["train_acc"] > target:
+            return r["eps"], "accuracy above target"
+    for a, b in zip(rows, rows[1:]):
+        # "the same in the first three digits": 90.21% and 90.26% agree (902)
+        if int(a["train_acc"] * 1000) == int(b["train_acc"] * 1000):
+            return a["eps"], "accuracy settled in three digits"
+    return rows[-1]["eps"], "smallest eps"
+
+
+def sweep(X, y, X_test, y_test, kernel="linear", gamma=1.0, coef0=0.0, degree=1, C=1.0,
+          eps_list=None, max_iter=0, on_row=None, on_start=None):
+    """Train for each eps (device tensors in, one dict per eps out); on_start and
+    on_row, if given, are called before each training and with each finished row."""
+    import torch
+
+    from . import _binding as B
+    eps_list = eps_list or DEFAULT_EPS
+    n, d = X.shape
+    kw = dict(kernel=kernel, gamma=gamma, coef0=coef0, degree=degree)
+    ws = B.alloc_workspace(B.workspace_bytes(n, d, X.dtype), X.device)
+    wsp_tr = B.alloc_workspace(B.predict_workspace_bytes(n, n, d, X.dtype), X.device)
+    wsp_te = B.alloc_workspace(B.predict_workspace_bytes(n, X_test.shape[0], d, X.dtype),
+                               X.device)
+    rows = []
+    for eps in eps_list:
+        if on_start is not None:
+            on_start(eps)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        r = B.train(X, y, C=C, eps=eps, max_iter=max_iter, workspace=ws, **kw)
+        t_train = (time.perf_counter() - t0) * 1e3
+        _, lab_tr = B.predict(X, r.alpha, r.b, X, workspace=wsp_tr, **kw)
+        _, lab_te = B.predict(X, r.alpha, r.b, X_test, workspace=wsp_te, **kw)
+        rows.append({
+            "eps": eps, "iterations": r.iterations, "converged": r.converged,
+            "rel_residual": r.rel_residual, "time_ms": round(t_train, 3),
+            "cg_ms": round(r.t_cg_ms, 3), "b": r.b,
+            "train_acc": float((lab_tr.to(y.dtype) == y).double().mean()),
+            "test_acc": float((lab_te.to(y_test.dtype) == y_test).double().mean()),
+            "alpha": r.alpha,
+        })
+        if on_row is not None:
+            on_row(rows[-1])
+    return rows
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--n", type=int, default=32768)
+    ap.add_argument("--d", type=int, default=4096)
+    ap.add_argument("--n-test", type=int, default=1024)
+    ap.add_argument("--kernel", default="linear", choices=["linear", "poly", "rbf"])
+    ap.add_argument("--dtype", default="f64", choices=["f64", "f32"])
+    ap.add_argument("--C", type=float, default=1.0)
+    ap.add_argument("--eps-min-exp", type=int, default=15)
+    ap.add_argument("--max-iter", type=int, default=500,
+                    help="CG iteration cap per eps (rows that hit it report converged=false)")
+    args = ap.parse_args(argv)
+
+    import torch
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    import synthdata as S
+
+    kparams = {"linear": {}, "poly": dict(gamma=1.0 / args.d, coef0=1.0, degree=3),
+               "rbf": dict(gamma=1.0 / args.d)}[args.kernel]
+    cfg = S.Config(f"{args.kernel}_{args.dtype}_{args.n}x{args.d}", args.dtype, args.kernel,
+                   args.n, args.d, mu=1.0, inf_frac=0.3, flip_frac=0.05, C=args.C, eps=1e-8,
+                   **kparams)
+    X, y, scale = S.make_train(cfg)
+    Xte, yte = S.make_test(cfg, scale, n_test=args.n_test)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(a).to(dev)  # noqa: E731
+    eps_list = [10.0 ** (-k) for k in range(1, args.eps_min_exp + 1)]
+    print(f"[eps_sweep] {cfg.name}: data on the device, {len(eps_list)} trainings",
+          file=sys.stderr, flush=True)
+
+    def emit(row):
+        print(json.dumps({"workload": cfg.name, **{k: v for k, v in row.items() if k != "alpha"}}),
+              flush=True)
+
+    rows = sweep(t(X), t(y), t(Xte), t(yte), kernel=args.kernel, C=args.C, eps_list=eps_list,
+                 max_iter=args.max_iter, on_row=emit, on_start=lambda e: print(
+                     f"[eps_sweep] training at eps={e:.0e}", file=sys.stderr, flush=True),
+                 **kparams)
+    eps_star, why = tune_eps(rows)
+    print(json.dumps({"workload": cfg.name, "tuned_eps": eps_star, "rule": why}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -423,3 +423,51 @@ def test_predict_linear_shortcut_large(torch_dev, dtype):
     assert rel_err(scores.cpu().numpy(), f_ref) <= tol * 10
     bad, _ = labels_match(labels.cpu().numpy(), f_ref, tol * 10)
     assert bad == 0
+
+
+def test_eps_sweep_matches_oracle(torch_dev):
+    """The eps sweep (Sec. IV-F) against the oracle run at every eps: iterations,
+    training and test accuracy, the eps the Sec. IV-B protocol picks, the
+    distance between the two solutions within C (||r_gpu|| + ||r_oracle||) at
+    every eps, and alpha~ within the bar once CG has converged tightly (mid-run
+    CG iterates are as sensitive to rounding as the oracle's own spread shows)."""
+    torch, dev = torch_dev
+    from paper_2202_12674_amd.eps_sweep import sweep, tune_eps
+    cfg = small_cfg("linear", "f64", 1024, 256)
+    X, y, Xte, yte = data_of(cfg)
+    eps_list = [10.0 ** (-k) for k in range(1, 13)]
+    rows = sweep(to_dev(torch, dev, X), to_dev(torch, dev, y), to_dev(torch, dev, Xte),
+                 to_dev(torch, dev, yte), kernel="linear", C=1.0, eps_list=eps_list)
+    spec = O.KernelSpec("linear")
+    Qt, q, Qmm = O.reduced_matrix(X, spec, 1.0)
+    rhs = O.reduced_rhs(y)
+    h = (cfg.n - 1) // 3
+    ref_rows = []
+    for eps, r in zip(eps_list, rows):
+        a_ref, b_ref, info = O.train(X, y, spec, 1.0, eps)
+        # mid-trajectory CG iterates are sensitive to rounding: the oracle's own
+        # spread under a change of summation order sets the alpha~ tolerance
+        alt = O.solve_cg(lambda v: Qt[:, :h] @ v[:h] + Qt[:, h:] @ v[h:], rhs, eps)
+        a_alt, _ = O.recover(alt.x, y, q, Qmm)
+        spread = np.abs(a_alt[:-1] - a_ref[:-1]).max() / np.abs(a_ref).max()
+        f_tr = O.decision(X, a_ref, b_ref, X, spec)
+        f_te = O.decision(X, a_ref, b_ref, Xte, spec)
+        acc_tr = float(np.mean(np.where(f_tr > 0, 1, -1) == y))
+        acc_te = float(np.mean(np.where(f_te > 0, 1, -1) == yte))
+        ref_rows.append({"eps": eps, "train_acc": acc_tr})
+        alpha = r["alpha"].cpu().numpy()
+        e = np.abs(alpha[:-1] - a_ref[:-1]).max() / np.abs(a_ref).max()
+        log(f"  eps {eps:.0e}: it {r['iterations']} (oracle {info['iterations']}), "
+            f"alpha~ err {e:.1e} (oracle order spread {spread:.1e}), "
+            f"train acc {r['train_acc']:.4f} ({acc_tr:.4f}), "
+            f"test acc {r['test_acc']:.4f} ({acc_te:.4f}), {r['time_ms']:.2f} ms")
+        assert r["converged"]
+        assert abs(r["iterations"] - info["iterations"]) <= max(2, info["iterations"] // 10)
+        # rigorous at every eps: both are within C ||r||_2 of the exact solution
+        r_gpu = np.linalg.norm(rhs - Qt @ alpha[:-1])
+        r_ref = np.linalg.norm(rhs - Qt @ a_ref[:-1])
+        assert np.linalg.norm(alpha[:-1] - a_ref[:-1]) <= 1.0 * (r_gpu + r_ref) * (1 + 1e-9)
+        if eps <= 1e-8:   # converged tightly: the trajectories agree again
+            assert e <= max(1e-9, 4 * spread)
+        assert r["train_acc"] == acc_tr and r["test_acc"] == acc_te
+    assert tune_eps(rows) == tune_eps(ref_rows)
