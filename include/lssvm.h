@@ -80,7 +80,8 @@ typedef struct lssvm_info {
     double true_rel_residual;      /* ||rhs - Q~ x|| / ||rhs|| if requested, else -1  */
     double t_setup_ms;             /* layout, q-vector, right-hand side               */
     double t_cg_ms;                /* CG loop                                         */
-    double t_total_ms;             /* whole call                                      */
+    double t_total_ms;             /* whole training (without the optional true-
+                                      residual product)                              */
     int32_t compute_true_residual; /* in: nonzero -> one extra product at the end     */
     int32_t reserved;
     double* residual_history;      /* in: host array or NULL; receives r^T r / r0^T r0

@@ -18,7 +18,6 @@ import argparse
 import json
 import os
 import sys
-import time
 
 DEFAULT_EPS = [10.0 ** (-k) for k in range(1, 16)]
 
@@ -57,14 +56,16 @@ def sweep(X, y, X_test, y_test, kernel="linear", gamma=1.0, coef0=0.0, degree=1,
         if on_start is not None:
             on_start(eps)
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        r = B.train(X, y, C=C, eps=eps, max_iter=max_iter, workspace=ws, **kw)
-        t_train = (time.perf_counter() - t0) * 1e3
+        # the true residual of the returned iterate costs one more product, which
+        # the library leaves out of t_total_ms
+        r = B.train(X, y, C=C, eps=eps, max_iter=max_iter, workspace=ws, true_residual=True, **kw)
+        t_train = r.t_total_ms
         _, lab_tr = B.predict(X, r.alpha, r.b, X, workspace=wsp_tr, **kw)
         _, lab_te = B.predict(X, r.alpha, r.b, X_test, workspace=wsp_te, **kw)
         rows.append({
             "eps": eps, "iterations": r.iterations, "converged": r.converged,
-            "rel_residual": r.rel_residual, "time_ms": round(t_train, 3),
+            "rel_residual": r.rel_residual, "true_rel_residual": r.true_rel_residual,
+            "time_ms": round(t_train, 3),
             "cg_ms": round(r.t_cg_ms, 3), "b": r.b,
             "train_acc": float((lab_tr.to(y.dtype) == y).double().mean()),
             "test_acc": float((lab_te.to(y_test.dtype) == y_test).double().mean()),
