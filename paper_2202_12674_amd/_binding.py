@@ -67,6 +67,26 @@ _SIGS = {
                                     ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "lssvm_last_error": (ctypes.c_char_p, []),
+    # host file IO (include/lssvm_io.h)
+    "lssvm_libsvm_scan": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
+                                         ctypes.POINTER(ctypes.c_int64), ctypes.c_int32]),
+    "lssvm_libsvm_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_int32]),
+    "lssvm_libsvm_write": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_int32]),
+    "lssvm_model_write": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.POINTER(Params), ctypes.c_double,
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_int64, ctypes.c_int64, ctypes.c_int32]),
+    "lssvm_model_scan": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int32),
+                                        ctypes.POINTER(Params), ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64),
+                                        ctypes.POINTER(ctypes.c_int64)]),
+    "lssvm_model_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_int32, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_int64, ctypes.c_int32]),
     "lssvm_tile_size": (ctypes.c_int32, [ctypes.c_int32]),
 }
 

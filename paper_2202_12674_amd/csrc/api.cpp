@@ -3,6 +3,7 @@
 // (Eq. (15)). Every numeric step runs in the gfx950 kernels of kernels.hip;
 // this file only validates, sequences launches and reads back scalars.
 #include "lssvm.h"
+#include "lssvm_error.h"
 #include "lssvm_internal.h"
 
 #include <hip/hip_runtime.h>
@@ -17,7 +18,6 @@
 #include <string>
 
 namespace lssvm {
-namespace {
 
 thread_local std::string g_last_error;
 
@@ -30,6 +30,10 @@ int fail(int code, const char* fmt, ...) {
   g_last_error = buf;
   return code;
 }
+
+void clear_error() { g_last_error.clear(); }
+
+namespace {
 
 #define LSSVM_HIP(call)                                                                  \
   do {                                                                                   \
