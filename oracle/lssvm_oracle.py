@@ -46,7 +46,7 @@ import scipy.linalg as sla
 __all__ = [
     "KernelSpec", "kernel_matrix", "kernel_rows", "bordered_matrix",
     "reduced_parts", "reduced_matrix", "reduced_rows", "reduced_rhs", "matvec_dense",
-    "matvec_rows", "solve_cholesky", "CGResult", "solve_cg", "recover",
+    "matvec_rows", "solve_cholesky", "CGResult", "solve_cg", "cg_step", "recover",
     "train", "decision", "predict", "full_system_residual",
 ]
 
@@ -310,6 +310,25 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
         d = r + (delta / delta_old) * d
     true_res = float(np.linalg.norm(b - matvec(x)) / np.linalg.norm(b))
     return CGResult(x, it, converged, float(np.sqrt(delta / delta0)), true_res, nmv, hist)
+
+
+def cg_step(x, r, d, q, rr):
+    """One CG iteration given q = A d (Sec. III-B, the steps of solve_cg without
+    the product and the stop test): returns x, r, d, r^T r, d^T q, step, beta.
+    On curvature breakdown (d^T q <= 0 or a non-finite step) the vectors are
+    returned unchanged with r^T r kept and beta = 0."""
+    x, r, d, q = (_f64(v).copy() for v in (x, r, d, q))
+    gamma = float(d @ q)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        step = float(np.float64(rr) / np.float64(gamma))
+    if not (gamma > 0.0) or not np.isfinite(step):
+        return x, r, d, float(rr), gamma, step, 0.0
+    x += step * d
+    r -= step * q
+    rr_new = float(r @ r)
+    beta = rr_new / rr
+    d = r + beta * d
+    return x, r, d, rr_new, gamma, step, beta
 
 
 def recover(alpha_t, y, q, Qmm):

@@ -444,3 +444,60 @@ def test_generator_recipe():
     assert abs(int((y > 0).sum()) - 2048) <= round(0.05 * 4096)
     Xt, yt = S.make_test(cfg, scale)
     assert Xt.shape == (1024, 1024)
+
+
+# ---------------------------------------------------------------- cg_step ---
+
+def test_cg_step_worked_example():
+    """A = diag(2, 1), b = (1, 1), x0 = 0, worked by hand: gamma = 3, a = 2/3,
+    x = (2/3, 2/3), r = (-1/3, 1/3), r^T r = 2/9, beta = 1/9, d = (-2/9, 4/9)."""
+    A = np.diag([2.0, 1.0])
+    b = np.array([1.0, 1.0])
+    d = b.copy()
+    x, r, d, rr, gamma, step, beta = O.cg_step(np.zeros(2), b, d, A @ d, float(b @ b))
+    assert gamma == 3.0 and abs(step - 2 / 3) < 1e-16
+    np.testing.assert_allclose(x, [2 / 3, 2 / 3], rtol=0, atol=1e-16)
+    np.testing.assert_allclose(r, [-1 / 3, 1 / 3], rtol=0, atol=1e-16)
+    assert abs(rr - 2 / 9) < 1e-16 and abs(beta - 1 / 9) < 1e-16
+    np.testing.assert_allclose(d, [-2 / 9, 4 / 9], rtol=0, atol=1e-16)
+
+
+def test_cg_step_textbook_properties():
+    """Iterated steps: residuals mutually orthogonal, directions A-conjugate,
+    r_k = b - A x_k, and the exact solution after n steps (finite termination)."""
+    rng = np.random.default_rng(21)
+    n = 12
+    M = rng.standard_normal((n, n))
+    A = M @ M.T + n * np.eye(n)
+    b = rng.standard_normal(n)
+    x, r, d = np.zeros(n), b.copy(), b.copy()
+    rr = float(b @ b)
+    rs, ds = [r.copy()], [d.copy()]
+    for _ in range(n):
+        x, r, d, rr, gamma, step, beta = O.cg_step(x, r, d, A @ d, rr)
+        assert gamma > 0
+        np.testing.assert_allclose(r, b - A @ x, rtol=0, atol=1e-10 * np.abs(b).max())
+        rs.append(r.copy())
+        ds.append(d.copy())
+    R = np.array(rs[:n])
+    D = np.array(ds[:n])
+    G = R @ R.T
+    off = G - np.diag(np.diag(G))
+    assert np.abs(off).max() <= 1e-9 * np.abs(np.diag(G)).max()
+    H = D @ A @ D.T
+    off = H - np.diag(np.diag(H))
+    assert np.abs(off).max() <= 1e-9 * np.abs(np.diag(H)).max()
+    np.testing.assert_allclose(x, np.linalg.solve(A, b), rtol=1e-9, atol=1e-12)
+
+
+def test_cg_step_breakdown_leaves_vectors():
+    x, r = np.ones(3), np.full(3, 2.0)
+    d = np.zeros(3)
+    out = O.cg_step(x, r, d, np.zeros(3), 12.0)
+    np.testing.assert_array_equal(out[0], x)
+    np.testing.assert_array_equal(out[1], r)
+    np.testing.assert_array_equal(out[2], d)
+    assert out[3] == 12.0 and out[4] == 0.0 and out[6] == 0.0
+    out = O.cg_step(x, r, np.ones(3), -np.ones(3), 12.0)       # negative curvature
+    np.testing.assert_array_equal(out[0], x)
+    assert out[4] == -3.0 and out[6] == 0.0
