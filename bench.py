@@ -10,9 +10,10 @@ Prints one JSON line. `value` is the whole-step throughput in GFLOP/s with
 the symmetric count N(N+1)d per implicit product (N = n - 1) plus
 2 n_test n d for the prediction. `roofline` is the tile kernel's own rate:
 N(N+1)d divided by its average duration, measured with HIP events recorded
-on the launch stream over the timed steps. `cpu_baseline` times the CPU
-oracle's explicit row-panel product on a bounded sample of the same
-workload.
+on the launch stream over the timed steps. `a5_cg_vector_step` times the CG
+vector step alone (lssvm_cg_step, 11 passes of N doubles) on N = 2^26 against
+the HBM peak. `cpu_baseline` times the CPU oracle's explicit row-panel product
+on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -90,6 +91,44 @@ def cpu_baseline(cfg, X, budget_s: float):
                       f"panels of {panel}) times a vector, {dt:.1f} s"}
 
 
+def a5_standalone(torch, dev, N: int, reps: int = 20):
+    """The CG vector step (lssvm_cg_step: d^T q, update, direction; 8 reads and
+    3 writes of N doubles) on vectors of length N, timed per step with HIP
+    events on the launch stream; the state is restored between steps."""
+    import paper_2202_12674_amd as P
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    x0 = torch.randn(N, dtype=torch.float64, device=dev, generator=g)
+    r0 = torch.randn(N, dtype=torch.float64, device=dev, generator=g)
+    d0 = torch.randn(N, dtype=torch.float64, device=dev, generator=g)
+    q = d0 * torch.rand(N, dtype=torch.float64, device=dev, generator=g).add_(0.5)
+    x, r, d = x0.clone(), r0.clone(), d0.clone()
+    rr0 = float(r0.dot(r0))
+    sc = torch.zeros(4, dtype=torch.float64, device=dev)
+    ws = P.alloc_workspace(P.lib().lssvm_cg_step_workspace_bytes(N), dev)
+    times = []
+    for k in range(reps + 3):
+        x.copy_(x0)
+        r.copy_(r0)
+        d.copy_(d0)
+        sc[0] = rr0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        P.cg_step(x, r, d, q, sc, workspace=ws)
+        e1.record()
+        e1.synchronize()
+        if k >= 3:
+            times.append(e0.elapsed_time(e1))
+    if float(sc[1]) <= 0.0:
+        raise RuntimeError("a5 measurement broke down (d^T q <= 0)")
+    ms = statistics.median(times)
+    nbytes = 11 * 8 * N
+    return {"N": N, "ms_per_step": round(ms, 4), "bytes_per_step": nbytes,
+            "achieved_GBs": round(nbytes / (ms * 1e-3) / 1e9, 1), "peak_GBs": HBM_GBS,
+            "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_GBS, 4),
+            "cov": round(statistics.pstdev(times) / statistics.mean(times), 4), "reps": reps}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -99,6 +138,10 @@ def main():
     ap.add_argument("--n-test", type=int, default=1024)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--a5-n", type=int, default=1 << 26,
+                    help="vector length of the standalone CG vector-step measurement (0: skip)")
+    ap.add_argument("--only-a5", action="store_true",
+                    help="only the standalone CG vector-step measurement (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (3 times) and exit: the "
                          "reference kernel for scaling HBM byte counters")
@@ -123,6 +166,11 @@ def main():
 
     import paper_2202_12674_amd as P
     import synthdata as S
+
+    if args.only_a5:
+        print(json.dumps({"a5_cg_vector_step": a5_standalone(torch, torch.device("cuda:0"),
+                                                             args.a5_n)}), flush=True)
+        return
 
     cfg = S.CONFIGS[args.config]
     dev = torch.device("cuda:0")
@@ -206,6 +254,10 @@ def main():
                      "traffic": traffic},
         "kernel_source_hash": kernel_source_hash(),
     }
+    del ws, wsp
+    if args.a5_n > 0:
+        log(f"[bench] CG vector step on N = {args.a5_n}")
+        line["a5_cg_vector_step"] = a5_standalone(torch, dev, args.a5_n)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         line["cpu_baseline"] = cpu_baseline(cfg, X, args.cpu_seconds)

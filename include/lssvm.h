@@ -152,6 +152,37 @@ int lssvm_matvec(const void* X, int64_t n, int64_t d, int32_t dtype, int32_t ker
                  const lssvm_params* kp, double C, const void* p, void* out,
                  void* workspace, size_t workspace_bytes, void* stream);
 
+/* Device workspace needed by lssvm_cg_step on vectors of length N (0 if N is
+ * out of range). */
+size_t lssvm_cg_step_workspace_bytes(int64_t N);
+
+/*
+ * One conjugate-gradient iteration (Sec. III-B) on caller-held fp64 device
+ * vectors of length N, for callers that apply the symmetric positive definite
+ * operator A themselves (for instance a product spread over several devices):
+ * with q = A d already computed,
+ *     gamma = d^T q,  a = rr / gamma,  x += a d,  r -= a q,
+ *     rr' = r^T r,    beta = rr' / rr, d = r + beta d.
+ * This is the vector work of one iteration of lssvm_train, in the same
+ * kernels (three passes over the vectors: 8 reads and 3 writes of N doubles).
+ *
+ * x, r, d    device, N doubles each, updated in place; q device, N doubles,
+ *            read. The four must not overlap.
+ * scalars    device, 4 doubles: in [0] = rr (r^T r of the current iterate);
+ *            out [0] = rr', [1] = gamma, [2] = a, [3] = beta. On curvature
+ *            breakdown (gamma <= 0 or a not finite) x, r and d are left as
+ *            they were, [0] keeps rr and [3] is 0.
+ * workspace  device, lssvm_cg_step_workspace_bytes(N) bytes, 256-byte aligned;
+ *            its contents need not survive between calls.
+ * stream     HIP stream (NULL = default). Everything is enqueued; nothing is
+ *            read back, so calls can follow each other without a host wait.
+ *            Calls that share a workspace must not run concurrently.
+ * Returns LSSVM_OK or LSSVM_EINVAL (NULL or aliased vectors, N < 1 or above
+ * 2^34, workspace) before any GPU work, or LSSVM_EHIP.
+ */
+int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, double* scalars,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
 /* Message for the last failing call on this thread ("" if none). The pointer
  * stays valid until the next call on this thread. */
 const char* lssvm_last_error(void);

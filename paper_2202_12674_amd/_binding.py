@@ -66,6 +66,10 @@ _SIGS = {
                                     ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(Params),
                                     ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "lssvm_cg_step_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
+    "lssvm_cg_step": (ctypes.c_int, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "lssvm_last_error": (ctypes.c_char_p, []),
     # host file IO (include/lssvm_io.h)
     "lssvm_libsvm_scan": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
@@ -262,3 +266,22 @@ def matvec(X, p, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
                               _stream(X.device))
     _check(code)
     return out
+
+
+def cg_step(x, r, d, q, scalars, workspace=None):
+    """lssvm_cg_step: one CG iteration in place on fp64 device vectors given
+    q = A d; scalars (4 fp64 on the device) carries r^T r in and
+    (r^T r, d^T q, step, beta) out. Nothing is read back."""
+    torch = _torch()
+    N = x.numel()
+    for t, nm in ((x, "x"), (r, "r"), (d, "d"), (q, "q"), (scalars, "scalars")):
+        if t.dtype != torch.float64:
+            raise TypeError(f"{nm} must be float64")
+    if not (r.numel() == d.numel() == q.numel() == N) or scalars.numel() < 4:
+        raise ValueError("x, r, d, q need equal lengths and scalars 4 entries")
+    if workspace is None:
+        workspace = alloc_workspace(lib().lssvm_cg_step_workspace_bytes(N), x.device)
+    _check(lib().lssvm_cg_step(N, _dev_ptr(x, "x"), _dev_ptr(r, "r"), _dev_ptr(d, "d"),
+                               _dev_ptr(q, "q"), _dev_ptr(scalars, "scalars"),
+                               _dev_ptr(workspace, "workspace"), workspace.numel(),
+                               _stream(x.device)))

@@ -68,7 +68,7 @@ struct Geometry {
   int64_t d_pad;    // features, multiple of 2 bk
   int64_t nT;       // tiles per edge of the reduced system
   int64_t NP;       // nT * tile: padded length of every CG vector
-  int64_t nb;       // blocks of 256 over NP
+  int64_t nb;       // blocks of the CG vector kernels over NP (block partials per reduction)
 };
 
 template <typename T>
@@ -83,7 +83,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.d_pad = round_up(d, 2 * g.bk);   // an even number of feature blocks (two LDS stages)
   g.nT = (g.N + g.tile - 1) / g.tile;
   g.NP = g.nT * g.tile;
-  g.nb = (g.NP + 255) / 256;
+  g.nb = vec_blocks(g.NP);
   return g;
 }
 
@@ -522,6 +522,29 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   return status;
 }
 
+// Workspace of lssvm_cg_step: the scalar area and two block-partial arrays.
+constexpr int64_t kMaxStepLen = int64_t(1) << 34;
+struct StepWs {
+  double *scal, *bp0, *bp1;
+  size_t bytes;
+};
+StepWs carve_step(int64_t N, void* base) {
+  Carver c(base);
+  StepWs w{};
+  const int64_t nb = vec_blocks(N);
+  w.scal = c.take<double>(S_COUNT);
+  w.bp0 = c.take<double>(nb + 1);
+  w.bp1 = c.take<double>(nb + 1);
+  w.bytes = c.off;
+  return w;
+}
+
+bool overlaps(const void* a, const void* b, int64_t bytes) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + bytes && pb < pa + bytes;
+}
+
 template <typename T>
 int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_params& kp,
                 double C, const T* p, T* out, void* workspace, size_t ws_bytes, hipStream_t s) {
@@ -618,6 +641,33 @@ lssvm_params params_or_default(const lssvm_params* kp) {
 using namespace lssvm;
 
 extern "C" {
+
+size_t lssvm_cg_step_workspace_bytes(int64_t N) {
+  if (N < 1 || N > kMaxStepLen) return 0;
+  return carve_step(N, nullptr).bytes;
+}
+
+int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, double* scalars,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    g_last_error.clear();
+    if (!x || !r || !d || !q || !scalars) return fail(LSSVM_EINVAL, "NULL array argument");
+    if (N < 1 || N > kMaxStepLen)
+      return fail(LSSVM_EINVAL, "N must be in [1, 2^34] (got %lld)", (long long)N);
+    const void* v[4] = {x, r, d, q};
+    for (int i = 0; i < 4; ++i)
+      for (int j = i + 1; j < 4; ++j)
+        if (overlaps(v[i], v[j], N * (int64_t)sizeof(double)))
+          return fail(LSSVM_EINVAL, "x, r, d and q must not overlap");
+    StepWs w = carve_step(N, workspace);
+    LSSVM_TRY(check_workspace(workspace, workspace_bytes, w.bytes));
+    LSSVM_HIP(launch_cg_step(N, x, r, d, q, scalars, w.scal, w.bp0, w.bp1,
+                             static_cast<hipStream_t>(stream)));
+    return LSSVM_OK;
+  } catch (...) {
+    return fail(LSSVM_EHIP, "internal error");
+  }
+}
 
 size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype) {
   if (n < 1 || d < 1 || !valid_dtype(dtype)) return 0;

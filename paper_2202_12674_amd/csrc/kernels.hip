@@ -465,22 +465,23 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
                                                   double* rhs, double* x, double* r, double* dir,
                                                   double* bpart, int* flags) {
   __shared__ double sh[NT / 64];
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   const double ym = (double)y[N];
-  double v = 0.0;
-  if (i < N) {
-    const double yi = (double)y[i];
-    if (!(yi == 1.0 || yi == -1.0)) flags[F_BADLABEL] = 1;
-    v = yi - ym;
-  }
-  if (i == 0 && !(ym == 1.0 || ym == -1.0)) flags[F_BADLABEL] = 1;
-  if (i < NP) {
+  if (blockIdx.x == 0 && threadIdx.x == 0 && !(ym == 1.0 || ym == -1.0)) flags[F_BADLABEL] = 1;
+  double acc = 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
+    double v = 0.0;
+    if (i < N) {
+      const double yi = (double)y[i];
+      if (!(yi == 1.0 || yi == -1.0)) flags[F_BADLABEL] = 1;
+      v = yi - ym;
+    }
     rhs[i] = v;
     x[i] = 0.0;
     r[i] = v;
     dir[i] = v;
+    acc += v * v;
   }
-  const double s = block_sum(v * v, sh);
+  const double s = block_sum(acc, sh);
   if (threadIdx.x == 0) bpart[blockIdx.x] = s;
 }
 
@@ -510,21 +511,21 @@ __global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ pa
                                                    double* bpart, const double* scal) {
   __shared__ double sh[NT / 64];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double prod = 0.0;
-  if (i < NP) {
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
     for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
     if (i >= N) s = 0.0;
     qv[i] = s;
-    prod = dir[i] * s;
+    prod += dir[i] * s;
   }
   const double t = block_sum(prod, sh);
   if (threadIdx.x == 0) bpart[blockIdx.x] = t;
 }
 
 // x += a d and r -= a q (or only x += a d when the residual is about to be
-// recomputed from x).
+// recomputed from x). On curvature breakdown (d^T q <= 0 or a step that is
+// not finite) every block leaves the vectors as they are.
 __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __restrict__ bp_in,
                                                    int64_t nb, double* scal, int par,
                                                    const double* __restrict__ dir,
@@ -535,24 +536,25 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
   const double gam = sum_partials(bp_in, nb, sh);
   const double delta = scal[S_DHIST + par];
   const double alpha = delta / gam;
+  const bool broke = !(gam > 0.0) || !__builtin_isfinite(alpha);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_ALPHA] = alpha;
     scal[S_GAMMA] = gam;
-    if (!(gam > 0.0) || !__builtin_isfinite(alpha)) {   // curvature breakdown
+    if (broke) {
       scal[S_STATUS + ST_CURV] = gam;
       scal[S_STATUS + ST_STEP] = alpha;
       scal[S_STATUS + ST_BREAK] = 1.0;
       scal[S_STATUS + ST_DONE] = 1.0;
     }
   }
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  if (broke) return;
   double v = 0.0;
-  if (i < NP) {
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     x[i] += alpha * dir[i];
     if (!x_only) {
       const double ri = r[i] - alpha * qv[i];
       r[i] = ri;
-      v = ri * ri;
+      v += ri * ri;
     }
   }
   if (!x_only) {
@@ -568,14 +570,13 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
                                                      double* bp_out, const double* scal) {
   __shared__ double sh[NT / 64];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double v = 0.0;
-  if (i < NP) {
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
     for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
     const double ri = i < N ? rhs[i] - s : 0.0;
     r[i] = ri;
-    v = ri * ri;
+    v += ri * ri;
   }
   const double t = block_sum(v, sh);
   if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
@@ -587,13 +588,12 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
                                                        const double* __restrict__ rhs,
                                                        double* bp_out) {
   __shared__ double sh[NT / 64];
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   double v = 0.0;
-  if (i < N) {
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
     for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
     const double ri = rhs[i] - s;
-    v = ri * ri;
+    v += ri * ri;
   }
   const double t = block_sum(v, sh);
   if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
@@ -612,8 +612,8 @@ __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__
   const double dnew = sum_partials(bp_in, nb, sh);
   const double dold = scal[S_DHIST + par];
   const double beta = dnew / dold;
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i < NP) dir[i] = r[i] + beta * dir[i];
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
+    dir[i] = r[i] + beta * dir[i];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_DHIST + (par ^ 1)] = dnew;
     st[ST_DELTA] = dnew;
@@ -622,6 +622,42 @@ __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__
     st[ST_ITER] = (double)iter;
     if (iter <= hist_cap) hist[iter - 1] = dnew;
     if (dnew <= st[ST_STOP]) st[ST_DONE] = 1.0;
+  }
+}
+
+// ------------------------------------------------- a5 on caller vectors -----
+// One CG iteration on vectors the caller holds, with q = A d supplied: the
+// caller's scalars[0] (r^T r) enters the double-buffered slot, the status is
+// cleared with a stop threshold no r^T r reaches, and after the update and
+// direction kernels the new r^T r, d^T q, step and beta go back to scalars.
+__global__ void k_step_begin(const double* scalars, double* scal) {
+  if (threadIdx.x == 0) {
+    scal[S_DHIST + 0] = scalars[0];
+    scal[S_DHIST + 1] = scalars[0];
+    for (int k = 0; k < ST_COUNT; ++k) scal[S_STATUS + k] = 0.0;
+    scal[S_STATUS + ST_STOP] = -1.0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_dot_partials(const double* __restrict__ a,
+                                                      const double* __restrict__ b, int64_t len,
+                                                      double* bp_out) {
+  __shared__ double sh[NT / 64];
+  double v = 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < len; i += (int64_t)gridDim.x * NT)
+    v += a[i] * b[i];
+  const double t = block_sum(v, sh);
+  if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+}
+
+__global__ void k_step_end(const double* scal, double* scalars) {
+  if (threadIdx.x == 0) {
+    const bool broke = scal[S_STATUS + ST_BREAK] != 0.0;
+    const double rr_old = scal[S_DHIST + 0], rr_new = scal[S_DHIST + 1];
+    scalars[0] = broke ? rr_old : rr_new;
+    scalars[1] = scal[S_GAMMA];
+    scalars[2] = scal[S_ALPHA];
+    scalars[3] = broke ? 0.0 : rr_new / rr_old;
   }
 }
 
@@ -840,7 +876,7 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
                            double* dir, double* bpart, int* flags, hipStream_t s) {
-  hipLaunchKernelGGL(k_rhs_init<T>, dim3(blocks_for(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
+  hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
                      dir, bpart, flags);
   return hipGetLastError();
 }
@@ -854,7 +890,7 @@ hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, d
 hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
                             const double* dir, double* qv, double* bpart, const double* scal,
                             hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_gather, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N, dir,
+  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N, dir,
                      qv, bpart, scal);
   return hipGetLastError();
 }
@@ -862,7 +898,7 @@ hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int6
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_update, dim3(blocks_for(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
+  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
                      par, dir, qv, x, r, bp_out, NP);
   return hipGetLastError();
 }
@@ -870,14 +906,14 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_residual, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N,
+  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N,
                      rhs, r, bp_out, scal);
   return hipGetLastError();
 }
 
 hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                                 const double* rhs, double* bp_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_true_residual, dim3(blocks_for(NP)), dim3(NT), 0, s, part, nslots, NP, N,
+  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N,
                      rhs, bp_out);
   return hipGetLastError();
 }
@@ -885,8 +921,22 @@ hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, 
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
                                double* hist, int64_t hist_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_direction, dim3(blocks_for(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
+  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
                      iter, r, dir, NP, hist, hist_cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_cg_step(int64_t N, double* x, double* r, double* d, const double* q,
+                          double* scalars, double* scal, double* bp0, double* bp1,
+                          hipStream_t s) {
+  const int64_t nb = vec_blocks(N);
+  hipLaunchKernelGGL(k_step_begin, dim3(1), dim3(64), 0, s, scalars, scal);
+  hipLaunchKernelGGL(k_dot_partials, dim3((unsigned)nb), dim3(NT), 0, s, d, q, N, bp0);
+  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)nb), dim3(NT), 0, s, 0, bp0, nb, scal, 0, d, q,
+                     x, r, bp1, N);
+  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)nb), dim3(NT), 0, s, bp1, nb, scal, 0,
+                     (int64_t)1, r, d, N, (double*)nullptr, (int64_t)0);
+  hipLaunchKernelGGL(k_step_end, dim3(1), dim3(64), 0, s, scal, scalars);
   return hipGetLastError();
 }
 

@@ -29,12 +29,6 @@ enum Kern : int { KLIN = 0, KPOLY = 1, KRBF = 2 };
 #endif
 constexpr int kNumXcd = 8;
 
-// Feature blocks in flight per workgroup in the tile kernel's register prefetch.
-#ifndef LSSVM_PREFETCH
-#define LSSVM_PREFETCH 2
-#endif
-constexpr int kPrefetch = LSSVM_PREFETCH;
-
 template <typename T> struct TileShape;
 template <> struct TileShape<float> { static constexpr int T = 128, BK = LSSVM_F32_BK; };
 template <> struct TileShape<double> { static constexpr int T = 128, BK = LSSVM_F64_BK; };
@@ -55,7 +49,18 @@ enum Scalar : int {
   S_COUNT = 16
 };
 enum StatusField : int { ST_DELTA = 0, ST_CURV = 1, ST_STEP = 2, ST_ITER = 3, ST_DONE = 4,
-                         ST_BREAK = 5, ST_STOP = 6, ST_COUNT = 8 };// Flags raised by kernels (int32 each).
+                         ST_BREAK = 5, ST_STOP = 6, ST_COUNT = 8 };
+
+// The CG vector kernels run at most this many blocks of 256 threads (4 per
+// CU), each striding over the vector, so every block can re-sum the previous
+// kernel's block partials cheaply at any vector length.
+constexpr int64_t kVecBlocks = 1024;
+inline int64_t vec_blocks(int64_t len) {
+  const int64_t b = (len + 255) / 256;
+  return b < kVecBlocks ? (b > 0 ? b : 1) : kVecBlocks;
+}
+
+// Flags raised by kernels (int32 each).
 enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
 template <typename T>
@@ -106,6 +111,11 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s);
+// One CG iteration on caller vectors of length N given q = A d: the scalars
+// (device, 4 doubles) carry r^T r in and r^T r, d^T q, step, beta out.
+hipError_t launch_cg_step(int64_t N, double* x, double* r, double* d, const double* q,
+                          double* scalars, double* scal, double* bp0, double* bp1,
+                          hipStream_t s);
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
                                double* hist, int64_t hist_cap, hipStream_t s);

@@ -144,3 +144,25 @@ def test_last_error_is_thread_local():
     t.join()
     assert seen["msg"] == ""
     assert "n must" in P.last_error()
+
+
+def test_cg_step_rejects_bad_arguments():
+    L = P.lib()
+    assert L.lssvm_cg_step_workspace_bytes(0) == 0
+    assert L.lssvm_cg_step_workspace_bytes(1 << 35) == 0
+    small = L.lssvm_cg_step_workspace_bytes(1000)
+    assert 0 < small < L.lssvm_cg_step_workspace_bytes(1 << 30)
+    v = [ctypes.c_void_p(4096 * k) for k in range(1, 6)]
+    N = 100
+
+    def call(N=N, x=v[0], r=v[1], d=v[2], q=v[3], sc=v[4], ws=ALIGNED_WS, wsb=1 << 20):
+        return L.lssvm_cg_step(N, x, r, d, q, sc, ws, wsb, None)
+
+    assert call(x=None) == B.EINVAL and "NULL" in P.last_error()
+    assert call(sc=None) == B.EINVAL
+    assert call(N=0) == B.EINVAL and "N must" in P.last_error()
+    assert call(N=1 << 35) == B.EINVAL
+    assert call(q=v[0]) == B.EINVAL and "overlap" in P.last_error()
+    assert call(r=ctypes.c_void_p(4096 + 8 * 50)) == B.EINVAL     # r inside x
+    assert call(ws=None) == B.EINVAL
+    assert call(wsb=8) == B.EINVAL and "too small" in P.last_error()
