@@ -129,6 +129,41 @@ def a5_standalone(torch, dev, N: int, reps: int = 20):
             "cov": round(statistics.pstdev(times) / statistics.mean(times), 4), "reps": reps}
 
 
+def cpu_phases(cfg, X, y, X_test, n_sub: int):
+    """The oracle's phases (Q~ assembly, Cholesky factor + solve, CG with the
+    explicit Q~, prediction) on the first n_sub points of the workload, timed
+    with time.perf_counter."""
+    import numpy as np
+    import oracle as O
+    spec = O.KernelSpec(cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+    Xs, ys = X[:n_sub].astype(np.float64), y[:n_sub].astype(np.float64)
+    out = {"sample": f"first {n_sub} points of the workload ({n_sub} x {cfg.d}, fp64), "
+                     f"{len(X_test)} test points"}
+    t = time.perf_counter()
+    Qt, q, Qmm = O.reduced_matrix(Xs, spec, cfg.C)
+    out["assembly_s"] = round(time.perf_counter() - t, 4)
+    rhs = O.reduced_rhs(ys)
+    t = time.perf_counter()
+    O.solve_cholesky(Qt, rhs)
+    out["cholesky_s"] = round(time.perf_counter() - t, 4)
+    t = time.perf_counter()
+    res = O.solve_cg(lambda v: O.matvec_dense(Qt, v), rhs, cfg.eps)
+    out["cg_s"] = round(time.perf_counter() - t, 4)
+    out["cg_iterations"] = res.iterations
+    alpha, b = O.recover(res.x, ys, q, Qmm)
+    t = time.perf_counter()
+    O.predict(Xs, alpha, b, X_test, spec)
+    out["predict_s"] = round(time.perf_counter() - t, 4)
+    return out
+
+
+def device_facts(torch, dev):
+    p = torch.cuda.get_device_properties(dev)
+    return {"name": p.name, "compute_units": p.multi_processor_count,
+            "hbm_gib": round(p.total_memory / 2**30, 1),
+            "arch": getattr(p, "gcnArchName", "")}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +175,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--a5-n", type=int, default=1 << 26,
                     help="vector length of the standalone CG vector-step measurement (0: skip)")
+    ap.add_argument("--cpu-phase-points", type=int, default=4096,
+                    help="points of the workload for the oracle's per-phase timing (0: skip)")
+    ap.add_argument("--only-peak", choices=["f32", "f64"],
+                    help="only the matrix-core loop peak probe for one dtype (for profiling)")
     ap.add_argument("--only-a5", action="store_true",
                     help="only the standalone CG vector-step measurement (for profiling)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -167,6 +206,11 @@ def main():
     import paper_2202_12674_amd as P
     import synthdata as S
 
+    if args.only_peak:
+        dt = torch.float32 if args.only_peak == "f32" else torch.float64
+        print(json.dumps({"measured_loop_peak_tflops": P.mfma_peak(dt, torch.device("cuda:0")),
+                          "dtype": args.only_peak}), flush=True)
+        return
     if args.only_a5:
         print(json.dumps({"a5_cg_vector_step": a5_standalone(torch, torch.device("cuda:0"),
                                                              args.a5_n)}), flush=True)
@@ -223,6 +267,8 @@ def main():
     mv_ms = sum(r.t_matvec_ms for r in results) / max(1, sum(r.n_matvec_timed for r in results))
     achieved = mv_flops / (mv_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[cfg.dtype]
+    measured_peak = P.mfma_peak(Xd.dtype, dev)
+    log(f"[bench] measured matrix-core loop peak {measured_peak:.1f} TFLOP/s")
     traffic = traffic_record(cfg.name)
     train_ms = [r.t_total_ms for r in results]
     line = {
@@ -251,7 +297,9 @@ def main():
         "matvec_dense_equiv_gflops": round(2 * N * N * cfg.d / (mv_ms * 1e-3) / 1e9, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                     "traffic": traffic},
+                     "traffic": traffic, "measured_loop_peak": round(measured_peak, 2),
+                     "frac_of_measured_loop_peak": round(achieved / measured_peak, 4)},
+        "device": device_facts(torch, dev),
         "kernel_source_hash": kernel_source_hash(),
     }
     del ws, wsp
@@ -261,6 +309,10 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         line["cpu_baseline"] = cpu_baseline(cfg, X, args.cpu_seconds)
+        if args.cpu_phase_points > 0:
+            log("[bench] timing the CPU oracle phases")
+            line["cpu_baseline"]["phases"] = cpu_phases(cfg, X, y, Xte,
+                                                        min(args.cpu_phase_points, cfg.n))
     print(json.dumps(line), flush=True)
 
 

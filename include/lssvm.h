@@ -183,6 +183,22 @@ size_t lssvm_cg_step_workspace_bytes(int64_t N);
 int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, double* scalars,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/* Device workspace of lssvm_mfma_peak (a fixed size). */
+size_t lssvm_mfma_peak_workspace_bytes(void);
+
+/*
+ * Sustained matrix-core rate in TFLOP/s of the instruction the tile kernel
+ * uses for dtype (fp32: v_mfma_f32_32x32x2_f32, fp64: v_mfma_f64_16x16x4_f64),
+ * measured by a kernel that issues only that instruction on every SIMD, with
+ * HIP events on `stream` (one warm-up launch, median of three). A measurement
+ * aid: it sets the tile kernel's rate against what the chip sustains, beside
+ * the published peak. workspace: device, lssvm_mfma_peak_workspace_bytes()
+ * bytes, 256-byte aligned (overwritten). Synchronizes `stream`.
+ * Returns LSSVM_OK, LSSVM_EINVAL or LSSVM_EHIP.
+ */
+int lssvm_mfma_peak(int32_t dtype, void* workspace, size_t workspace_bytes, double* tflops_out,
+                    void* stream);
+
 /* Message for the last failing call on this thread ("" if none). The pointer
  * stays valid until the next call on this thread. */
 const char* lssvm_last_error(void);

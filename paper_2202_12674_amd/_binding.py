@@ -70,6 +70,9 @@ _SIGS = {
     "lssvm_cg_step": (ctypes.c_int, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "lssvm_mfma_peak_workspace_bytes": (ctypes.c_size_t, []),
+    "lssvm_mfma_peak": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]),
     "lssvm_last_error": (ctypes.c_char_p, []),
     # host file IO (include/lssvm_io.h)
     "lssvm_libsvm_scan": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
@@ -285,3 +288,15 @@ def cg_step(x, r, d, q, scalars, workspace=None):
                                _dev_ptr(q, "q"), _dev_ptr(scalars, "scalars"),
                                _dev_ptr(workspace, "workspace"), workspace.numel(),
                                _stream(x.device)))
+
+
+def mfma_peak(dtype, device) -> float:
+    """lssvm_mfma_peak: sustained TFLOP/s of the tile kernel's matrix-core
+    instruction for dtype (torch.float32 or torch.float64) on device."""
+    torch = _torch()
+    code = F64 if dtype == torch.float64 else F32
+    ws = alloc_workspace(lib().lssvm_mfma_peak_workspace_bytes(), device)
+    out = ctypes.c_double(0.0)
+    _check(lib().lssvm_mfma_peak(code, _dev_ptr(ws, "workspace"), ws.numel(), ctypes.byref(out),
+                                 _stream(device)))
+    return out.value

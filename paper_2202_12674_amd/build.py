@@ -23,7 +23,7 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
-SOURCES = ["kernels.hip", "api.cpp", "io.cpp"]
+SOURCES = ["kernels.hip", "probe.hip", "api.cpp", "io.cpp"]
 
 
 def hipcc() -> str:

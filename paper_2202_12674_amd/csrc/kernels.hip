@@ -71,9 +71,6 @@ template <typename T> struct TileCfg {
   static constexpr int BM = TileShape<T>::T;
   static constexpr int BK = TileShape<T>::BK;
   static constexpr int WM = BM / 2, WN = BM / 2;
-  static constexpr int PAD = 16 / sizeof(T);  // LDS row padding: one 16-byte vector,
-                                              // which makes the row pitch 36 banks
-                                              // (conflict-free 16-byte reads)
 };
 
 template <typename T> __device__ inline T texp(T x);

@@ -166,3 +166,16 @@ def test_cg_step_rejects_bad_arguments():
     assert call(r=ctypes.c_void_p(4096 + 8 * 50)) == B.EINVAL     # r inside x
     assert call(ws=None) == B.EINVAL
     assert call(wsb=8) == B.EINVAL and "too small" in P.last_error()
+
+
+def test_mfma_peak_rejects_bad_arguments():
+    L = P.lib()
+    assert L.lssvm_mfma_peak_workspace_bytes() >= 512 * 256 * 8
+    out = ctypes.c_double()
+    assert L.lssvm_mfma_peak(3, ALIGNED_WS, 1 << 30, ctypes.byref(out), None) == B.EINVAL
+    assert L.lssvm_mfma_peak(1, None, 1 << 30, ctypes.byref(out), None) == B.EINVAL
+    assert L.lssvm_mfma_peak(1, ctypes.c_void_p(4100), 1 << 30, ctypes.byref(out), None) \
+        == B.EINVAL and "aligned" in P.last_error()
+    assert L.lssvm_mfma_peak(1, ALIGNED_WS, 1024, ctypes.byref(out), None) == B.EINVAL
+    assert "too small" in P.last_error()
+    assert L.lssvm_mfma_peak(0, ALIGNED_WS, 1 << 30, None, None) == B.EINVAL

@@ -547,3 +547,15 @@ def test_cg_step_breakdown_keeps_vectors(torch_dev):
     assert torch.all(x == 1.0) and torch.all(r == 2.0) and torch.all(d == 1.0)
     got = sc.cpu().numpy()
     assert got[0] == 7.0 and got[1] == -float(n) and got[3] == 0.0
+
+
+@pytest.mark.parametrize("dtype,published", [("float32", 157.3), ("float64", 78.6)])
+def test_mfma_peak_probe_is_plausible(torch_dev, dtype, published):
+    """The measured matrix-core loop rate lies near the published peak (one
+    resident round of back-to-back MFMAs sustains ~99% of it on gfx950) and
+    not above it (a probe that lost its work would report far more)."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    tf = P.mfma_peak(getattr(torch, dtype), dev)
+    log(f"[mfma peak] {dtype}: {tf:.1f} TFLOP/s (published {published})")
+    assert 0.9 * published < tf < 1.02 * published
