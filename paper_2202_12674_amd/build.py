@@ -24,6 +24,8 @@ HIP_FLAGS = [
     "-Wall", "-Wno-unused-function",
 ]
 SOURCES = ["kernels.hip", "probe.hip", "api.cpp", "io.cpp"]
+BIN = os.path.join(PKG, "bin")
+TOOLS = [("lssvm_train.cpp", "lssvm-train"), ("lssvm_predict.cpp", "lssvm-predict")]
 
 
 def hipcc() -> str:
@@ -54,6 +56,16 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB_PATH)
+    # command-line tools over the C ABI, next to the library they load
+    os.makedirs(BIN, exist_ok=True)
+    for src, exe in TOOLS:
+        out = os.path.join(BIN, exe)
+        cmd = [cc, "-O2", "-std=c++17", "-Wall", "-I", INCLUDE, os.path.join(CSRC, "tools", src),
+               "-L", PKG, "-llssvm", "-Wl,-rpath,$ORIGIN/..", "-o", out + ".tmp"]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(out + ".tmp", out)
     return LIB_PATH
 
 
