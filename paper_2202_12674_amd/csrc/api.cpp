@@ -14,6 +14,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 
@@ -50,6 +51,16 @@ namespace {
   } while (0)
 
 constexpr size_t kAlign = 256;
+
+// LSSVM_LOG=1 in the environment: one stderr line per batch of CG iterations
+// and one per finished training (read once per process).
+bool log_enabled() {
+  static const bool on = [] {
+    const char* v = std::getenv("LSSVM_LOG");
+    return v && *v && std::strcmp(v, "0") != 0;
+  }();
+  return on;
+}
 constexpr int64_t kReplaceEvery = 50;  // residual recomputed every 50th iteration
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
@@ -468,6 +479,10 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
       break;
     }
     delta = st[ST_DELTA];
+    if (log_enabled())
+      std::fprintf(stderr, "[lssvm] CG iteration %lld: relative residual %.3e (%.1f ms)\n",
+                   (long long)it, delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0,
+                   ms_since(t1));
     batch = std::min<int64_t>(2 * batch, 32);
   }
   const bool converged = done && !broke;
@@ -496,6 +511,12 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   *b_out = g_host.p[0];
 
   const double t_total = ms_since(t0);   // the optional true-residual product is not training
+  if (log_enabled())
+    std::fprintf(stderr,
+                 "[lssvm] train n=%lld d=%lld: %lld iterations, relative residual %.3e, "
+                 "setup %.2f ms, cg %.2f ms, total %.2f ms\n",
+                 (long long)n, (long long)d, (long long)it,
+                 delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0, t_setup, t_cg, t_total);
   if (info) {
     info->iterations = it;
     info->rel_residual = delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0;

@@ -66,3 +66,25 @@ def test_train_and_predict_tools(tmp_path, kernel, flag, dtype, n, d, eps):
     acc = float((labels == yte.astype(np.int64)).mean())
     m = re.search(r"Accuracy = ([0-9.]+)%", r.stdout)
     assert m and abs(float(m.group(1)) - 100 * acc) < 1e-3
+
+
+def test_train_log_lines(tmp_path):
+    """LSSVM_LOG=1 makes the training runtime report each batch of CG
+    iterations and the finished training on stderr; unset, it stays silent."""
+    from paper_2202_12674_amd import files as F
+    cfg = S.Config("cli_log", "f64", "rbf", 200, 10, mu=1.0, inf_frac=0.5, flip_frac=0.05,
+                   C=1.0, eps=1e-10, gamma=0.1)
+    X, y, _ = S.make_train(cfg)
+    train = str(tmp_path / "train.libsvm")
+    F.write(train, X, y)
+    exe = os.path.join(BIN, "lssvm-train")
+    args = [exe, "-t", "2", "-g", "0.1", "-e", "1e-10", "-q", train, str(tmp_path / "m")]
+    r = subprocess.run(args, capture_output=True, text=True, timeout=120,
+                       env=dict(os.environ, LSSVM_LOG="1"))
+    assert r.returncode == 0, r.stderr
+    its = [int(m) for m in re.findall(r"\[lssvm\] CG iteration (\d+): relative residual", r.stderr)]
+    assert its and its == sorted(its)
+    assert re.search(r"\[lssvm\] train n=200 d=10: \d+ iterations", r.stderr)
+    env = {k: v for k, v in os.environ.items() if k != "LSSVM_LOG"}
+    r = subprocess.run(args, capture_output=True, text=True, timeout=120, env=env)
+    assert r.returncode == 0 and "[lssvm]" not in r.stderr
