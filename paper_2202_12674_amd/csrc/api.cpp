@@ -239,13 +239,16 @@ struct MatvecTimer {
     for (auto& e : ev)
       if (e) (void)hipEventDestroy(e);
   }
+  // A batch queues at most 32 iterations of at most two products each, so the
+  // pairs never run out; should they, the extra products are simply not timed.
+  bool full() const { return used >= kPairs; }
   hipError_t start(hipStream_t s, int64_t iter) {
-    if (!on) return hipSuccess;
+    if (!on || full()) return hipSuccess;
     tag[used] = iter;
     return hipEventRecord(ev[2 * used], s);
   }
   hipError_t stop(hipStream_t s) {
-    if (!on) return hipSuccess;
+    if (!on || full()) return hipSuccess;
     hipError_t r = hipEventRecord(ev[2 * used + 1], s);
     ++used;
     return r;
