@@ -267,13 +267,17 @@ class CGResult:
 
 
 def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
-             replace_every: int = 50) -> CGResult:
+             replace_every: int = 50, x0=None) -> CGResult:
     """Conjugate gradients for the SPD reduced system (Sec. III-B).
 
     matvec(v) returns Q~ v. Steps per iteration, in Shewchuk's notation:
     q = A d; alpha = delta / d^T q; x += alpha d; r -= alpha q (or r = b - A x
     every ``replace_every`` iterations); delta_new = r^T r; stop once
     delta_new <= eps^2 delta_0; beta = delta_new / delta_old; d = r + beta d.
+
+    x0 (optional) is a starting iterate: r = b - A x0 (one product). delta_0
+    stays b^T b, so the stop test is relative to the right-hand side wherever
+    CG starts. A zero right-hand side returns x = 0 whatever x0 is.
     """
     b = _f64(rhs)
     N = b.shape[0]
@@ -281,13 +285,20 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
         max_iter = N
     x = np.zeros(N)
     r = b.copy()
-    d = r.copy()
-    delta = float(r @ r)
-    delta0 = delta
+    delta0 = float(b @ b)
     hist = []
     nmv = 0
     if delta0 == 0.0:
         return CGResult(x, 0, True, 0.0, 0.0, 0, hist)
+    if x0 is not None:
+        x = _f64(x0).copy()
+        r = b - matvec(x)
+        nmv += 1
+    d = r.copy()
+    delta = float(r @ r)
+    if delta <= eps * eps * delta0:
+        true_res = float(np.linalg.norm(b - matvec(x)) / np.linalg.norm(b))
+        return CGResult(x, 0, True, float(np.sqrt(delta / delta0)), true_res, nmv, hist)
     converged = False
     it = 0
     while it < max_iter:
@@ -346,10 +357,11 @@ def recover(alpha_t, y, q, Qmm):
 
 
 def train(X, y, spec: KernelSpec, C: float, eps: float, max_iter: int = 0,
-          method: str = "cg"):
+          method: str = "cg", alpha0=None):
     """Solve the LS-SVM for (alpha, b, info) by the reduced route of Sec. II-F.
 
     method "cg" follows Sec. III-B; "cholesky" is the direct dense solve.
+    alpha0 (optional, "cg" only): CG starts from its first n - 1 entries.
     """
     X = _f64(X)
     y = _f64(y)
@@ -362,7 +374,8 @@ def train(X, y, spec: KernelSpec, C: float, eps: float, max_iter: int = 0,
         at = solve_cholesky(Qt, rhs)
         info = {"iterations": 0, "converged": True}
     elif method == "cg":
-        res = solve_cg(lambda v: Qt @ v, rhs, eps, max_iter)
+        x0 = None if alpha0 is None else _f64(alpha0)[:-1]
+        res = solve_cg(lambda v: Qt @ v, rhs, eps, max_iter, x0=x0)
         at = res.x
         info = dataclasses.asdict(res)
         del info["x"]

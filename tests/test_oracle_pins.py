@@ -501,3 +501,54 @@ def test_cg_step_breakdown_leaves_vectors():
     out = O.cg_step(x, r, np.ones(3), -np.ones(3), 12.0)       # negative curvature
     np.testing.assert_array_equal(out[0], x)
     assert out[4] == -3.0 and out[6] == 0.0
+
+
+# ------------------------------------------------------------- warm start ---
+
+def _spd_case(seed=31, n=40, d=6, C=1.0):
+    rng = np.random.default_rng(seed)
+    X = rng.uniform(-1, 1, (n, d))
+    y = np.where(rng.random(n) < 0.5, 1.0, -1.0)
+    spec = O.KernelSpec("rbf", gamma=0.5)
+    Qt, q, Qmm = O.reduced_matrix(X, spec, C)
+    return X, y, spec, Qt, O.reduced_rhs(y)
+
+
+def test_warm_start_from_the_solution_takes_no_iteration():
+    _, _, _, Qt, rhs = _spd_case()
+    xs = np.linalg.solve(Qt, rhs)
+    res = O.solve_cg(lambda v: Qt @ v, rhs, 1e-8, x0=xs)
+    assert res.iterations == 0 and res.converged
+    np.testing.assert_array_equal(res.x, xs)
+    assert res.n_matvec == 1
+
+
+def test_warm_start_from_zero_is_the_cold_start():
+    _, _, _, Qt, rhs = _spd_case()
+    cold = O.solve_cg(lambda v: Qt @ v, rhs, 1e-10)
+    warm = O.solve_cg(lambda v: Qt @ v, rhs, 1e-10, x0=np.zeros_like(rhs))
+    assert warm.iterations == cold.iterations
+    np.testing.assert_array_equal(warm.x, cold.x)
+
+
+def test_warm_start_meets_the_rigorous_bound():
+    """From a random start CG still stops at ||r|| <= eps ||rhs|| (the stop test
+    stays relative to the right-hand side), and ||x - x*|| <= C ||r|| (P9)."""
+    C = 2.0
+    _, _, _, Qt, rhs = _spd_case(C=C)
+    xs = np.linalg.solve(Qt, rhs)
+    x0 = np.random.default_rng(5).standard_normal(rhs.shape[0]) * 10
+    res = O.solve_cg(lambda v: Qt @ v, rhs, 1e-9, x0=x0)
+    assert res.converged and res.rel_residual <= 1e-9
+    r = rhs - Qt @ res.x
+    assert np.linalg.norm(res.x - xs) <= C * np.linalg.norm(r) * (1 + 1e-6)
+    assert res.true_rel_residual <= 1e-8
+
+
+def test_warm_start_with_zero_rhs_returns_zero():
+    X, _, spec, Qt, _ = _spd_case()
+    y = np.ones(X.shape[0])
+    alpha, b, info = O.train(X, y, spec, 1.0, 1e-8, alpha0=np.ones(X.shape[0]))
+    assert info["iterations"] == 0
+    np.testing.assert_array_equal(alpha, 0.0)
+    assert b == 1.0
