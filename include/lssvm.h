@@ -76,15 +76,16 @@ typedef struct lssvm_params {
 typedef struct lssvm_info {
     int64_t iterations;            /* CG iterations performed                        */
     int64_t n_matvec;              /* implicit Q~ products (incl. residual refreshes) */
-    double rel_residual;           /* sqrt(r^T r / r0^T r0) of the CG recurrence      */
+    double rel_residual;           /* sqrt(r^T r / rhs^T rhs) of the CG recurrence    */
     double true_rel_residual;      /* ||rhs - Q~ x|| / ||rhs|| if requested, else -1  */
     double t_setup_ms;             /* layout, q-vector, right-hand side               */
     double t_cg_ms;                /* CG loop                                         */
     double t_total_ms;             /* whole training (without the optional true-
                                       residual product)                              */
     int32_t compute_true_residual; /* in: nonzero -> one extra product at the end     */
-    int32_t reserved;
-    double* residual_history;      /* in: host array or NULL; receives r^T r / r0^T r0
+    int32_t warm_start;            /* in: nonzero -> CG starts from the first n-1
+                                      entries of alpha_out (see lssvm_train)         */
+    double* residual_history;      /* in: host array or NULL; receives r^T r / rhs^T rhs
                                       after each iteration                           */
     int64_t history_capacity;      /* in: length of residual_history                 */
     int32_t time_matvec;           /* in: nonzero -> time every Q~ product with HIP
@@ -111,9 +112,15 @@ size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32
  *           be NULL for LSSVM_LINEAR).
  * C         regularisation, finite and > 0.
  * eps       relative-residual target, 0 < eps < 1: CG stops once
- *           r^T r <= eps^2 r0^T r0 (x0 = 0, r0 = ybar - y_m 1).
+ *           r^T r <= eps^2 rhs^T rhs (rhs = ybar - y_m 1, the residual of x = 0).
  * max_iter  iteration cap; 0 means N = n - 1.
  * alpha_out device, n values, dtype: alpha~ followed by alpha_m = -sum(alpha~).
+ *           With info->warm_start set it is also an input: CG starts at x0 =
+ *           its first n - 1 entries (finite; a previous solution, or a saved
+ *           iterate to resume from) instead of 0, with r0 = rhs - Q~ x0 (one
+ *           more product, counted in n_matvec and t_cg_ms). The stop test stays
+ *           relative to rhs, so a start that already meets it returns after 0
+ *           iterations with alpha~ = x0 (alpha_m and b recomputed).
  * b_out     host, the bias of Eq. (15).
  * info      host, may be NULL.
  * CG details: the residual is recomputed as rhs - Q~ x every 50th iteration;

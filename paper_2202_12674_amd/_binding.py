@@ -32,7 +32,7 @@ class Info(ctypes.Structure):
                 ("rel_residual", ctypes.c_double), ("true_rel_residual", ctypes.c_double),
                 ("t_setup_ms", ctypes.c_double), ("t_cg_ms", ctypes.c_double),
                 ("t_total_ms", ctypes.c_double), ("compute_true_residual", ctypes.c_int32),
-                ("reserved", ctypes.c_int32),
+                ("warm_start", ctypes.c_int32),
                 ("residual_history", ctypes.POINTER(ctypes.c_double)),
                 ("history_capacity", ctypes.c_int64), ("time_matvec", ctypes.c_int32),
                 ("reserved2", ctypes.c_int32), ("t_matvec_ms", ctypes.c_double),
@@ -198,8 +198,12 @@ class TrainResult:
 def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
           degree: int = 1, C: float = 1.0, eps: float = 1e-8, max_iter: int = 0,
           workspace=None, true_residual: bool = False, history: int = 0,
-          raise_not_converged: bool = False, time_matvec: bool = False) -> TrainResult:
-    """lssvm_train on device tensors X (n x d) and y (n,), same float dtype."""
+          raise_not_converged: bool = False, time_matvec: bool = False,
+          alpha0=None) -> TrainResult:
+    """lssvm_train on device tensors X (n x d) and y (n,), same float dtype.
+
+    alpha0 (device tensor, n values): start CG from its first n - 1 entries
+    (a previous solution or a saved iterate) instead of zero."""
     torch = _torch()
     n, d = X.shape
     dt = _dtype_code(X)
@@ -211,6 +215,11 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
     alpha = torch.empty(n, dtype=X.dtype, device=X.device)
     b = ctypes.c_double(0.0)
     info = Info()
+    if alpha0 is not None:
+        if alpha0.shape != (n,) or alpha0.dtype != X.dtype or alpha0.device != X.device:
+            raise ValueError("alpha0 must have shape (n,) and the dtype and device of X")
+        alpha.copy_(alpha0)
+        info.warm_start = 1
     info.compute_true_residual = 1 if true_residual else 0
     info.time_matvec = 1 if time_matvec else 0
     hist = (ctypes.c_double * history)() if history > 0 else None

@@ -449,6 +449,23 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   int status = LSSVM_OK;
   int64_t batch = 1;
   double* st = g_host.p;
+  int64_t warm_products = 0;
+  if (info && info->warm_start && !done) {
+    // x0 = the caller's alpha~, r0 = rhs - Q~ x0, dir = r0; the stop threshold
+    // set from rhs^T rhs above is kept
+    LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
+    LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.x, s));
+    LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+    LSSVM_HIP(launch_warm_start(w.bp1, g.nb, w.scal, w.r, w.dir, g.NP, s));
+    LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
+                             hipMemcpyDeviceToHost, s));
+    LSSVM_HIP(hipStreamSynchronize(s));
+    delta = st[ST_DELTA];
+    done = st[ST_DONE] != 0.0;
+    warm_products = 1;
+    if (!std::isfinite(delta))
+      return fail(LSSVM_ENONFINITE, "the warm-start alpha gives a non-finite residual");
+  }
   while (!done && queued < max_iter) {
     const int64_t nq = std::min<int64_t>(batch, max_iter - queued);
     for (int64_t b = 0; b < nq; ++b) {
@@ -489,7 +506,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     batch = std::min<int64_t>(2 * batch, 32);
   }
   const bool converged = done && !broke;
-  const int64_t nmv = it + it / kReplaceEvery;
+  const int64_t nmv = it + it / kReplaceEvery + warm_products;
   const double t_cg = ms_since(t1);
   if (status == LSSVM_OK && !converged) {
     status = LSSVM_NOT_CONVERGED;

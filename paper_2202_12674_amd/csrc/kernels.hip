@@ -635,6 +635,24 @@ __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__
   }
 }
 
+// After r = rhs - Q~ x0 for a warm start: r^T r becomes the current delta
+// (the stop threshold stays eps^2 rhs^T rhs), the direction starts at r, and
+// done is raised if x0 already meets the threshold.
+__global__ __launch_bounds__(256) void k_warm_start(const double* __restrict__ bp_in, int64_t nb,
+                                                    double* scal, const double* __restrict__ r,
+                                                    double* dir, int64_t NP) {
+  __shared__ double sh[NT / 64];
+  const double dlt = sum_partials(bp_in, nb, sh);
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
+    dir[i] = r[i];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    double* st = scal + S_STATUS;
+    scal[S_DHIST + 0] = dlt;
+    st[ST_DELTA] = dlt;
+    if (dlt <= st[ST_STOP]) st[ST_DONE] = 1.0;
+  }
+}
+
 // ------------------------------------------------- a5 on caller vectors -----
 // One CG iteration on vectors the caller holds, with q = A d supplied: the
 // caller's scalars[0] (r^T r) enters the double-buffered slot, the status is
@@ -933,6 +951,13 @@ hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, in
                                double* hist, int64_t hist_cap, hipStream_t s) {
   hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
                      iter, r, dir, NP, hist, hist_cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_warm_start(const double* bp_in, int64_t nb, double* scal, const double* r,
+                             double* dir, int64_t NP, hipStream_t s) {
+  hipLaunchKernelGGL(k_warm_start, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal,
+                     r, dir, NP);
   return hipGetLastError();
 }
 

@@ -111,6 +111,10 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s);
+// Warm start: delta = r0^T r0 from the block partials, dir = r0, done if
+// already below the stop threshold.
+hipError_t launch_warm_start(const double* bp_in, int64_t nb, double* scal, const double* r,
+                             double* dir, int64_t NP, hipStream_t s);
 // One CG iteration on caller vectors of length N given q = A d: the scalars
 // (device, 4 doubles) carry r^T r in and r^T r, d^T q, step, beta out.
 hipError_t launch_cg_step(int64_t N, double* x, double* r, double* d, const double* q,

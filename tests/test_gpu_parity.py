@@ -559,3 +559,66 @@ def test_mfma_peak_probe_is_plausible(torch_dev, dtype, published):
     tf = P.mfma_peak(getattr(torch, dtype), dev)
     log(f"[mfma peak] {dtype}: {tf:.1f} TFLOP/s (published {published})")
     assert 0.9 * published < tf < 1.02 * published
+
+
+# ------------------------------------------------------------- warm start ---
+
+def _alpha_err(a, ref):
+    a = np.asarray(a, dtype=np.float64)[:-1]
+    ref = np.asarray(ref, dtype=np.float64)[:-1]
+    return float(np.abs(a - ref).max() / np.abs(ref).max())
+
+
+@pytest.mark.parametrize("dtype,kernel,n,d", [("f64", "rbf", 500, 24), ("f32", "poly", 400, 64)])
+def test_warm_start_random_matches_oracle(torch_dev, dtype, kernel, n, d):
+    """CG from a random alpha~0: the oracle's warm CG from the same values."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=1.0)
+    X, y, _, _ = data_of(cfg)
+    a0 = (np.random.default_rng(9).standard_normal(n) * 0.05).astype(cfg.np_dtype)
+    ref_a, ref_b, info = O.train(X, y, spec_of(cfg), cfg.C, cfg.eps, alpha0=a0)
+    res = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=cfg.C, eps=cfg.eps,
+                  alpha0=to_dev(torch, dev, a0), **kw_of(cfg))
+    log(f"  warm {cfg.name}: it {res.iterations} (oracle {info['iterations']}) "
+        f"rel {res.rel_residual:.2e}")
+    assert res.converged and res.rel_residual <= cfg.eps
+    assert res.n_matvec == res.iterations + res.iterations // 50 + 1
+    if dtype == "f64":
+        assert abs(res.iterations - info["iterations"]) <= 2
+    else:
+        assert res.iterations <= 2 * info["iterations"] + 10
+    assert _alpha_err(res.alpha.cpu().numpy(), ref_a) <= TOL_ALPHA[dtype]
+
+
+def test_warm_start_resumes_at_a_tighter_eps(torch_dev):
+    """Solve at eps = 1e-4, then continue from that alpha to 1e-10: fewer
+    iterations than a cold run to 1e-10, the same solution within the bar;
+    restarting at the returned solution takes at most a couple of iterations."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("rbf", "f64", 600, 16, C=10.0, eps=1e-10)
+    X, y, _, _ = data_of(cfg)
+    Xd, yd = to_dev(torch, dev, X), to_dev(torch, dev, y)
+    coarse = P.train(Xd, yd, C=cfg.C, eps=1e-4, **kw_of(cfg))
+    cold = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, **kw_of(cfg))
+    warm = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, alpha0=coarse.alpha, **kw_of(cfg))
+    log(f"  coarse {coarse.iterations} it, cold {cold.iterations} it, resumed {warm.iterations} it")
+    assert warm.converged and warm.iterations < cold.iterations
+    ref_a, ref_b, _ = O.train(X, y, spec_of(cfg), cfg.C, cfg.eps)
+    assert _alpha_err(warm.alpha.cpu().numpy(), ref_a) <= 1e-8
+    again = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, alpha0=warm.alpha, **kw_of(cfg))
+    assert again.iterations <= 2 and again.converged
+    assert _alpha_err(again.alpha.cpu().numpy(), warm.alpha.cpu().numpy()) <= 1e-9
+
+
+def test_warm_start_equal_labels_still_zero(torch_dev):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("linear", "f64", 64, 5)
+    X, _, _, _ = data_of(cfg)
+    y = np.ones(cfg.n)
+    res = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=1.0, eps=1e-8,
+                  alpha0=torch.ones(cfg.n, dtype=torch.float64, device=dev), **kw_of(cfg))
+    assert res.iterations == 0 and res.b == 1.0
+    assert float(res.alpha.abs().max()) == 0.0
