@@ -38,8 +38,9 @@ def log(msg):
 
 
 def kernel_source_hash() -> str:
+    """Hash of the tile kernel's source (tiles.h and the shared internal header)."""
     h = hashlib.sha256()
-    for f in ("kernels.hip", "lssvm_internal.h"):
+    for f in ("tiles.h", "lssvm_internal.h"):
         with open(os.path.join(ROOT, "paper_2202_12674_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

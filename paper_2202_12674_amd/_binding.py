@@ -99,12 +99,20 @@ _SIGS = {
 
 
 def lib() -> ctypes.CDLL:
-    """The loaded HIP library; raises if it has not been built."""
+    """The loaded HIP library; raises if it has not been built.
+
+    torch is imported first: it ships its own HIP runtime, and the library's
+    libamdhip64 dependency must resolve to that same copy (two HIP runtimes in
+    one process do not share the device)."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with "
                               "`python -m paper_2202_12674_amd.build` (no CPU fallback exists)")
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in _SIGS.items():
             fn = getattr(L, name)
