@@ -38,9 +38,11 @@ def tune_eps(rows, target: float = 0.97):
 
 
 def sweep(X, y, X_test, y_test, kernel="linear", gamma=1.0, coef0=0.0, degree=1, C=1.0,
-          eps_list=None, max_iter=0, on_row=None, on_start=None):
+          eps_list=None, max_iter=0, on_row=None, on_start=None, warm=False):
     """Train for each eps (device tensors in, one dict per eps out); on_start and
-    on_row, if given, are called before each training and with each finished row."""
+    on_row, if given, are called before each training and with each finished row.
+    warm: start each eps from the previous eps's solution (continuation) instead
+    of from zero, as the paper does."""
     import torch
 
     from . import _binding as B
@@ -52,18 +54,22 @@ def sweep(X, y, X_test, y_test, kernel="linear", gamma=1.0, coef0=0.0, degree=1,
     wsp_te = B.alloc_workspace(B.predict_workspace_bytes(n, X_test.shape[0], d, X.dtype),
                                X.device)
     rows = []
+    prev = None
     for eps in eps_list:
         if on_start is not None:
             on_start(eps)
         torch.cuda.synchronize()
         # the true residual of the returned iterate costs one more product, which
         # the library leaves out of t_total_ms
-        r = B.train(X, y, C=C, eps=eps, max_iter=max_iter, workspace=ws, true_residual=True, **kw)
+        r = B.train(X, y, C=C, eps=eps, max_iter=max_iter, workspace=ws, true_residual=True,
+                    alpha0=prev if warm else None, **kw)
+        prev = r.alpha
         t_train = r.t_total_ms
         _, lab_tr = B.predict(X, r.alpha, r.b, X, workspace=wsp_tr, **kw)
         _, lab_te = B.predict(X, r.alpha, r.b, X_test, workspace=wsp_te, **kw)
         rows.append({
-            "eps": eps, "iterations": r.iterations, "converged": r.converged,
+            "eps": eps, "warm": bool(warm), "iterations": r.iterations,
+            "converged": r.converged,
             "rel_residual": r.rel_residual, "true_rel_residual": r.true_rel_residual,
             "time_ms": round(t_train, 3),
             "cg_ms": round(r.t_cg_ms, 3), "b": r.b,
@@ -87,6 +93,8 @@ def main(argv=None):
     ap.add_argument("--eps-min-exp", type=int, default=15)
     ap.add_argument("--max-iter", type=int, default=500,
                     help="CG iteration cap per eps (rows that hit it report converged=false)")
+    ap.add_argument("--warm", action="store_true",
+                    help="start each eps from the previous solution (not the paper's protocol)")
     args = ap.parse_args(argv)
 
     import torch
@@ -114,7 +122,7 @@ def main(argv=None):
               flush=True)
 
     rows = sweep(t(X), t(y), t(Xte), t(yte), kernel=args.kernel, C=args.C, eps_list=eps_list,
-                 max_iter=args.max_iter, on_row=emit, on_start=lambda e: print(
+                 max_iter=args.max_iter, warm=args.warm, on_row=emit, on_start=lambda e: print(
                      f"[eps_sweep] training at eps={e:.0e}", file=sys.stderr, flush=True),
                  **kparams)
     eps_star, why = tune_eps(rows)
