@@ -17,6 +17,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 namespace lssvm {
@@ -75,19 +76,21 @@ template <typename T, int BK, int TP>
 __global__ __launch_bounds__(256) void k_layout(const T* __restrict__ X, int64_t n, int64_t d,
                                                 T* __restrict__ Xb, int64_t ld, int64_t nkb,
                                                 int* __restrict__ flags) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= nkb * ld * BK) return;
-  const int64_t kk = idx % BK;
-  const int64_t r = (idx / BK) % TP;
-  const int64_t kb = (idx / ((int64_t)BK * TP)) % nkb;
-  const int64_t pb = idx / ((int64_t)BK * TP * nkb);
-  const int64_t i = pb * TP + r, k = kb * BK + kk;
-  T v = T(0);
-  if (i < n && k < d) {
-    v = X[i * d + k];
-    if (!__builtin_isfinite(v)) flags[F_NONFINITE] = 1;
+  const int64_t total = nkb * ld * BK;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t kk = idx % BK;
+    const int64_t r = (idx / BK) % TP;
+    const int64_t kb = (idx / ((int64_t)BK * TP)) % nkb;
+    const int64_t pb = idx / ((int64_t)BK * TP * nkb);
+    const int64_t i = pb * TP + r, k = kb * BK + kk;
+    T v = T(0);
+    if (i < n && k < d) {
+      v = X[i * d + k];
+      if (!__builtin_isfinite(v)) flags[F_NONFINITE] = 1;
+    }
+    Xb[idx] = v;
   }
-  Xb[idx] = v;
 }
 
 // ----------------------------------------------------------- a2 norms, q ----
@@ -515,8 +518,10 @@ hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, in
                          int* flags, hipStream_t s) {
   constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
   const int64_t total = d_pad * ld;
-  hipLaunchKernelGGL((k_layout<T, BK, TP>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                     s, X, n, d, Xt, ld, d_pad / BK, flags);
+  // grid-stride: the element count can exceed what one dispatch can count
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, int64_t(1) << 20);
+  hipLaunchKernelGGL((k_layout<T, BK, TP>), dim3((unsigned)blocks), dim3(256), 0, s, X, n, d, Xt,
+                     ld, d_pad / BK, flags);
   return hipGetLastError();
 }
 
@@ -544,26 +549,35 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
   return hipGetLastError();
 }
 
+// Workgroups per tile launch: 2^23 x 256 threads stays below the 2^32 work
+// items one dispatch can count; a multiple of 8, so every chunk starts on XCD 0.
+constexpr int64_t kMaxTileGrid = int64_t(1) << 23;
+
+template <typename T, bool SYM>
+hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t ntiles, hipStream_t s) {
+  a.ntiles = ntiles;
+  for (int64_t base = 0; base < ntiles; base += kMaxTileGrid) {
+    a.tile_base = base;
+    const dim3 grid((unsigned)std::min(kMaxTileGrid, ntiles - base));
+    switch (kernel) {
+      case KLIN: hipLaunchKernelGGL((k_tiles<T, SYM, KLIN>), grid, dim3(256), 0, s, a); break;
+      case KPOLY: hipLaunchKernelGGL((k_tiles<T, SYM, KPOLY>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((k_tiles<T, SYM, KRBF>), grid, dim3(256), 0, s, a); break;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 template <typename T>
 hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s) {
-  dim3 grid((unsigned)ntiles_1d);
-  switch (kernel) {
-    case KLIN: hipLaunchKernelGGL((k_tiles<T, true, KLIN>), grid, dim3(256), 0, s, a); break;
-    case KPOLY: hipLaunchKernelGGL((k_tiles<T, true, KPOLY>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((k_tiles<T, true, KRBF>), grid, dim3(256), 0, s, a); break;
-  }
-  return hipGetLastError();
+  return launch_tiles<T, true>(a, kernel, ntiles_1d, s);
 }
 
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s) {
-  dim3 grid((unsigned)(nTr * a.nTc));
-  switch (kernel) {
-    case KLIN: hipLaunchKernelGGL((k_tiles<T, false, KLIN>), grid, dim3(256), 0, s, a); break;
-    case KPOLY: hipLaunchKernelGGL((k_tiles<T, false, KPOLY>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((k_tiles<T, false, KRBF>), grid, dim3(256), 0, s, a); break;
-  }
-  return hipGetLastError();
+  return launch_tiles<T, false>(a, kernel, nTr * a.nTc, s);
 }
 
 template <typename T>

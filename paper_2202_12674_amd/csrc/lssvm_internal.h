@@ -82,6 +82,10 @@ struct TileArgs {
   double* part;  // partial sums, part[slot * part_ld + row]
   const double* status;  // symmetric mode: CG status (skip the launch once done) or null
   int64_t part_ld;
+  // A product's tiles may outnumber one launch (the dispatch grid counts work
+  // items in 32 bits), so the launcher splits them into chunks: workgroup b of
+  // a chunk takes tile slot tile_base + b of ntiles.
+  int64_t tile_base, ntiles;
 };
 
 template <typename T>

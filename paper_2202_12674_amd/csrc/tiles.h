@@ -150,21 +150,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     if (a.status && a.status[ST_DONE] != 0.0) return;   // CG already stopped
   }
   int64_t I, J;
+  const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's tile slot
   if constexpr (SYM) {
     if (a.order) {
-      // workgroup w runs on XCD w % 8: give each XCD a contiguous run of the order
-      const uint32_t G = gridDim.x, w = blockIdx.x;
-      const uint32_t x = w % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
-      const uint32_t slot = x * per + (x < extra ? x : extra) + w / kNumXcd;
+      // workgroup w runs on XCD w % 8 (chunks start at multiples of 8, so this
+      // holds for the slot t too): give each XCD a contiguous run of the order
+      const int64_t G = a.ntiles;
+      const int64_t x = t % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
+      const int64_t slot = x * per + (x < extra ? x : extra) + t / kNumXcd;
       const uint32_t packed = a.order[slot];
       I = packed >> 16;
       J = packed & 0xFFFFu;
     } else {
-      tri_index((int64_t)blockIdx.x, I, J);
+      tri_index(t, I, J);
     }
   } else {
-    I = (int64_t)blockIdx.x / a.nTc;
-    J = (int64_t)blockIdx.x % a.nTc;
+    I = t / a.nTc;
+    J = t % a.nTc;
   }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;

@@ -622,3 +622,71 @@ def test_warm_start_equal_labels_still_zero(torch_dev):
                   alpha0=torch.ones(cfg.n, dtype=torch.float64, device=dev), **kw_of(cfg))
     assert res.iterations == 0 and res.b == 1.0
     assert float(res.alpha.abs().max()) == 0.0
+
+
+# ---------------------------------------------------------- largest sizes ---
+
+@pytest.mark.parametrize("dtype,kernel,n,d", [("f32", "rbf", 1 << 20, 16),
+                                              ("f64", "linear", (1 << 19) + 77, 24)])
+def test_matvec_large_n_sampled_rows(torch_dev, dtype, kernel, n, d):
+    """The implicit product at n up to 2^20 points (33.6M tiles, a 69 GB
+    workspace of tile partials): sampled rows, including the last row and
+    the ragged last tile, against the oracle's rows computed one by one; over
+    all rows, p^T Q~ p > 0 (Q~ is SPD) and every entry finite."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    log(f"[large n] {kernel} {dtype} n={n} d={d}")
+    kw = dict(linear={}, rbf=dict(gamma=1.0 / d))[kernel]
+    cfg = S.Config(f"large_{kernel}", dtype, kernel, n, d, mu=1.0, inf_frac=0.5,
+                   flip_frac=0.05, C=1.0, eps=1e-6, **kw)
+    X, _, _ = S.make_train(cfg)
+    N = n - 1
+    p = S.probe_vector(N, cfg.np_dtype)
+    ws = P.alloc_workspace(P.workspace_bytes(n, d, getattr(torch, "float64" if dtype == "f64"
+                                                            else "float32")), dev)
+    log(f"  workspace {ws.numel() / 2**30:.1f} GiB")
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=cfg.C, workspace=ws,
+                   **kw_of(cfg))
+    torch.cuda.synchronize()
+    o = out.double().cpu().numpy()
+    del ws, out
+    torch.cuda.empty_cache()
+    assert np.isfinite(o).all()
+    assert float(p.astype(np.float64) @ o) > 0.0
+    rng = np.random.default_rng(n)
+    rows = np.unique(np.concatenate([[0, 1, N - 1, N - 2], N - 1 - np.arange(0, 300, 7),
+                                     rng.choice(N, 24, replace=False)]))
+    ref = O.reduced_rows(X.astype(np.float64), spec_of(cfg), cfg.C, rows) @ p.astype(np.float64)
+    err = float(np.abs(o[rows] - ref).max() / np.abs(ref).max())
+    log(f"  {len(rows)} sampled rows: max rel err {err:.2e}")
+    assert err <= TOL_MV[dtype]
+
+
+def test_predict_layout_beyond_one_dispatch(torch_dev):
+    """2^20 test points of 4100 fp32 features: their panel layout holds 4.4e9
+    elements, more than one dispatch can count, so the layout kernel strides.
+    Sampled decision values against the oracle; seeded inputs drawn on the
+    device."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    n, d, nt = 256, 4100, 1 << 20
+    log(f"[layout > 2^32] n={n} n_test={nt} d={d}")
+    g = torch.Generator(device=dev)
+    g.manual_seed(2024)
+    Xtr = torch.rand(n, d, dtype=torch.float32, device=dev, generator=g) * 2 - 1
+    Xte = torch.rand(nt, d, dtype=torch.float32, device=dev, generator=g) * 2 - 1
+    alpha = torch.randn(n, dtype=torch.float32, device=dev, generator=g)
+    gamma = 1.0 / d
+    scores, labels = P.predict(Xtr, alpha, 0.25, Xte, kernel="rbf", gamma=gamma)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, nt - 1, nt - 2],
+                                     np.random.default_rng(3).choice(nt, 20, replace=False)]))
+    idx = torch.from_numpy(rows).to(dev)
+    f_ref, lab_ref = O.predict(Xtr.double().cpu().numpy(), alpha.double().cpu().numpy(), 0.25,
+                               Xte[idx].double().cpu().numpy(), O.KernelSpec("rbf", gamma=gamma))
+    got = scores[idx].double().cpu().numpy()
+    err = float(np.abs(got - f_ref).max() / max(1.0, np.abs(f_ref).max()))
+    log(f"  sampled decision values: max rel err {err:.2e}")
+    assert err <= 2e-4
+    del Xte, scores, labels
+    torch.cuda.empty_cache()
