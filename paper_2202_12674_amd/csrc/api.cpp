@@ -115,9 +115,9 @@ template <typename T>
 struct TrainWs {
   T* Xt;
   T* norms;
-  T* qT;
   double* q64;
   double* part;
+  double* pq;   // per tile panel: sum p_j, then sum q_j p_j (2 nT)
   double *rhs, *x, *r, *dir, *qv;
   double *bp0, *bp1;
   double* scal;
@@ -149,9 +149,9 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   TrainWs<T> w{};
   w.Xt = c.take<T>(g.d_pad * g.ld);
   w.norms = c.take<T>(g.ld);
-  w.qT = c.take<T>(g.ld);
   w.q64 = c.take<double>(g.ld);
   w.part = c.take<double>(g.nT * g.NP);
+  w.pq = c.take<double>(2 * g.nT);
   w.rhs = c.take<double>(g.NP);
   w.x = c.take<double>(g.NP);
   w.r = c.take<double>(g.NP);
@@ -304,9 +304,15 @@ int check_workspace(const void* ws, size_t have, size_t need) {
   return LSSVM_OK;
 }
 
+// Exponent scale of the RBF tile epilogue: fp32 evaluates exp(-gamma dist)
+// as exp2(-(gamma log2 e) dist) on the hardware base-2 exponential.
+template <typename T> T rbf_scale(double gamma);
+template <> float rbf_scale<float>(double gamma) { return (float)(gamma * 1.4426950408889634); }
+template <> double rbf_scale<double>(double gamma) { return gamma; }
+
 template <typename T>
-TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                     double C, const double* p) {
+TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
+                     const double* p) {
   TileArgs<T> a{};
   a.A = w.Xt;
   a.B = w.Xt;
@@ -315,14 +321,13 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.nkb = g.d_pad / g.bk;
   a.nA = w.norms;
   a.nB = w.norms;
-  a.qA = w.qT;
-  a.qB = w.qT;
   a.pv = p;
+  a.q64 = w.q64;
+  a.pq = w.pq;
   a.gamma = (T)kp.gamma;
   a.coef0 = (T)kp.coef0;
+  a.rbf_scale = rbf_scale<T>(kp.gamma);
   a.degree = kp.degree;
-  a.qmm = (T)(kmm + 1.0 / C);
-  a.invC = (T)(1.0 / C);
   a.nTc = g.nT;
   a.order = LSSVM_TILE_GROUP > 0 ? w.order : nullptr;
   a.part = w.part;
@@ -341,39 +346,44 @@ int upload_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
   return LSSVM_OK;
 }
 
-// a1 + a2: layout, norms, q and k_mm; reads back k_mm and the input flags.
+// a1 + a2: layout, norms, q and k_mm (left on the device); reads back the
+// input flags.
 template <typename T>
 int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
-                 const lssvm_params& kp, hipStream_t s, double* kmm) {
+                 const lssvm_params& kp, hipStream_t s) {
   LSSVM_TRY(upload_order<T>(g, w, s));
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
   LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
-                              kp.degree, w.norms, w.qT, w.q64, w.scal, s));
+                              kp.degree, w.norms, w.q64, w.scal, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
-  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_KMM, sizeof(double), hipMemcpyDeviceToHost, s));
   LSSVM_HIP(hipStreamSynchronize(s));
   if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
-  *kmm = g_host.p[0];
   return LSSVM_OK;
 }
 
-// One implicit product Q~ p into the partial-sum buffer.
+// The terms of Q~ p that the tile partials leave out, for the vector p.
 template <typename T>
-int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                    double C, int32_t kernel, const double* p, hipStream_t s) {
-  TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
+RankOne rank_one(const Geometry& g, const TrainWs<T>& w, double C, const double* p) {
+  return RankOne{w.pq, g.nT, w.q64, p, w.scal, 1.0 / C};
+}
+
+// One implicit product K p into the partial-sum buffer (plus the per-panel
+// sums of the rank-one terms).
+template <typename T>
+int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
+                    int32_t kernel, const double* p, hipStream_t s) {
+  TileArgs<T> a = sym_args<T>(g, w, kp, p);
   LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT), s));
   return LSSVM_OK;
 }
 
 template <typename T>
-int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, double kmm,
-                 double C, int32_t kernel, const double* p, hipStream_t s, MatvecTimer& tm,
-                 int64_t iter) {
+int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, int32_t kernel,
+                 const double* p, hipStream_t s, MatvecTimer& tm, int64_t iter) {
   LSSVM_HIP(tm.start(s, iter));
-  TileArgs<T> a = sym_args<T>(g, w, kp, kmm, C, p);
+  TileArgs<T> a = sym_args<T>(g, w, kp, p);
   a.status = w.scal + S_STATUS;   // skip the launch once CG has stopped
   LSSVM_HIP(launch_tiles_sym<T>(a, kernel, g.nT * (g.nT + 1) / 2, s));
   LSSVM_HIP(tm.stop(s));
@@ -422,8 +432,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   }
 
   // ---- setup: a1, a2, a3
-  double kmm = 0.0;
-  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
+  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
   LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.bp0, w.flags, s));
   LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
@@ -454,8 +463,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     // x0 = the caller's alpha~, r0 = rhs - Q~ x0, dir = r0; the stop threshold
     // set from rhs^T rhs above is kept
     LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
-    LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.x, s));
-    LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+    LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
+    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
     LSSVM_HIP(launch_warm_start(w.bp1, g.nb, w.scal, w.r, w.dir, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
@@ -471,13 +480,13 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     for (int64_t b = 0; b < nq; ++b) {
       const int64_t k = ++queued;
       const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
-      LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.dir, s, tm, k));
-      LSSVM_HIP(launch_cg_gather(w.part, g.nT, g.NP, g.N, w.dir, w.qv, w.bp0, w.scal, s));
+      LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
+      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, C, w.dir), g.NP, g.N, w.qv, w.bp0, w.scal, s));
       if (k % kReplaceEvery == 0) {
         LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
-        LSSVM_TRY(timed_matvec<T>(g, w, kp, kmm, C, kernel, w.x, s, tm, k));
-        LSSVM_HIP(launch_cg_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+        LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.x, s, tm, k));
+        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
       } else {
         LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
@@ -543,8 +552,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     if (info->compute_true_residual) {
       double tr = 0.0;
       if (delta0 > 0.0) {
-        LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.x, s));
-        LSSVM_HIP(launch_true_residual(w.part, g.nT, g.NP, g.N, w.rhs, w.bp1, s));
+        LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
+        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.bp1, s));
         LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
         LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
                                  hipMemcpyDeviceToHost, s));
@@ -594,11 +603,10 @@ int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_pa
   LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
   w = carve_train<T>(g, workspace);
   LSSVM_HIP(g_host.ensure());
-  double kmm = 0.0;
-  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, &kmm));
+  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
   LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, s));
-  LSSVM_TRY(matvec_partials<T>(g, w, kp, kmm, C, kernel, w.dir, s));
-  LSSVM_HIP(launch_mv_out<T>(w.part, g.nT, g.NP, g.N, out, s));
+  LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.dir, s));
+  LSSVM_HIP(launch_mv_out<T>(w.part, rank_one(g, w, C, w.dir), g.NP, g.N, out, s));
   LSSVM_HIP(hipStreamSynchronize(s));
   return LSSVM_OK;
 }
@@ -627,9 +635,9 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   LSSVM_HIP(launch_layout<T>(Xte, n_test, d, w.Xte, w.ld_te, g.d_pad, w.flags, s));
   if (kernel == LSSVM_RBF) {  // squared norms are only read by the radial kernel
     LSSVM_HIP(launch_norms_q<T>(w.Xtr, g.ld, g.d_pad, -1, 0, kernel, kp.gamma, kp.coef0,
-                                kp.degree, w.ntr, nullptr, nullptr, nullptr, s));
+                                kp.degree, w.ntr, nullptr, nullptr, s));
     LSSVM_HIP(launch_norms_q<T>(w.Xte, w.ld_te, g.d_pad, -1, 0, kernel, kp.gamma, kp.coef0,
-                                kp.degree, w.nte, nullptr, nullptr, nullptr, s));
+                                kp.degree, w.nte, nullptr, nullptr, s));
   }
   LSSVM_HIP(launch_pad_vec<T>(alpha, n, w.alpha, g.ld, s));
   TileArgs<T> a{};
@@ -640,12 +648,10 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   a.nkb = g.d_pad / g.bk;
   a.nA = w.nte;
   a.nB = w.ntr;
-  a.qA = nullptr;
-  a.qB = nullptr;
-  a.pv = nullptr;
   a.wB = w.alpha;
   a.gamma = (T)kp.gamma;
   a.coef0 = (T)kp.coef0;
+  a.rbf_scale = rbf_scale<T>(kp.gamma);
   a.degree = kp.degree;
   a.nTc = w.nTc;
   a.part = w.part;

@@ -63,6 +63,23 @@ __device__ inline double sum_partials(const double* bp, int64_t nb, double* sh) 
   return block_sum(v, sh);
 }
 
+// Block-wide S, T and Q_mm of the rank-one terms (every block sums the
+// panel partials in the same order, so all blocks agree).
+struct RankOneSums {
+  double S, Tq, qmm;
+};
+__device__ inline RankOneSums rank_one_sums(const RankOne& c, double* sh) {
+  RankOneSums r;
+  r.S = sum_partials(c.pq, c.nT, sh);
+  r.Tq = sum_partials(c.pq + c.nT, c.nT, sh);
+  r.qmm = c.scal[S_KMM] + c.invC;
+  return r;
+}
+// (Q~ p)_i from the tile sum (K p)_i, for i < N.
+__device__ inline double qtilde_row(const RankOne& c, const RankOneSums& r, int64_t i, double kp) {
+  return kp + (r.qmm - c.q64[i]) * r.S - r.Tq + c.p[i] * c.invC;
+}
+
 // ------------------------------------------------------------- a1 layout ----
 // Panel-major, feature-blocked layout. Points are grouped in panels of TP
 // (the tile edge) and features in blocks of BK; panel pb holds its nkb blocks
@@ -100,7 +117,7 @@ template <typename T, int BK, int TP, int KER>
 __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64_t ld,
                                                  int64_t nkb, int64_t m, int64_t N, double gamma,
                                                  double coef0, int degree, T* __restrict__ norms,
-                                                 T* __restrict__ qT, double* __restrict__ q64,
+                                                 double* __restrict__ q64,
                                                  double* __restrict__ scal) {
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   if (i >= ld) return;
@@ -132,7 +149,6 @@ __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64
     const double kv = kernel_value64<KER>(dot, dist, gamma, coef0, degree);
     const double qv = i < N ? kv : 0.0;
     q64[i] = qv;
-    qT[i] = (T)qv;
     if (i == m) scal[S_KMM] = kv;
   }
 }
@@ -182,20 +198,23 @@ __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int6
 }
 
 // ------------------------------------------------------------- a5 CG --------
-// q = Q~ d from the tile partials (masked beyond N) and the block partials of d^T q.
-__global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ part, int64_t nslots,
-                                                   int64_t NP, int64_t N,
-                                                   const double* __restrict__ dir, double* qv,
+// q = Q~ d from the tile partials and the rank-one terms (zero beyond N),
+// and the block partials of d^T q (c.p = d).
+__global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ part, RankOne c,
+                                                   int64_t NP, int64_t N, double* qv,
                                                    double* bpart, const double* scal) {
   __shared__ double sh[NT / 64];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
+  const RankOneSums ro = rank_one_sums(c, sh);
   double prod = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
-    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
-    if (i >= N) s = 0.0;
+    if (i < N) {
+      for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+      s = qtilde_row(c, ro, i, s);
+    }
     qv[i] = s;
-    prod += dir[i] * s;
+    prod += c.p[i] * s;
   }
   const double t = block_sum(prod, sh);
   if (threadIdx.x == 0) bpart[blockIdx.x] = t;
@@ -241,18 +260,23 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
   }
 }
 
-// r = rhs - Q~ x from the tile partials, and the block partials of r^T r.
-__global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part,
-                                                     int64_t nslots, int64_t NP, int64_t N,
+// r = rhs - Q~ x from the tile partials (c.p = x), and the block partials
+// of r^T r.
+__global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part, RankOne c,
+                                                     int64_t NP, int64_t N,
                                                      const double* __restrict__ rhs, double* r,
                                                      double* bp_out, const double* scal) {
   __shared__ double sh[NT / 64];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
+  const RankOneSums ro = rank_one_sums(c, sh);
   double v = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
-    double s = 0.0;
-    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
-    const double ri = i < N ? rhs[i] - s : 0.0;
+    double ri = 0.0;
+    if (i < N) {
+      double s = 0.0;
+      for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+      ri = rhs[i] - qtilde_row(c, ro, i, s);
+    }
     r[i] = ri;
     v += ri * ri;
   }
@@ -262,15 +286,16 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
 
 // ||rhs - Q~ x||^2 partials without touching r (final report only).
 __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict__ part,
-                                                       int64_t nslots, int64_t NP, int64_t N,
+                                                       RankOne c, int64_t NP, int64_t N,
                                                        const double* __restrict__ rhs,
                                                        double* bp_out) {
   __shared__ double sh[NT / 64];
+  const RankOneSums ro = rank_one_sums(c, sh);
   double v = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
-    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
-    const double ri = rhs[i] - s;
+    for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+    const double ri = rhs[i] - qtilde_row(c, ro, i, s);
     v += ri * ri;
   }
   const double t = block_sum(v, sh);
@@ -469,13 +494,14 @@ __global__ __launch_bounds__(256) void k_pad_vec(const T* __restrict__ src, int6
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part, int64_t nslots,
+__global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part, RankOne c,
                                                 int64_t NP, int64_t N, T* __restrict__ out) {
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i < N) {
+  __shared__ double sh[NT / 64];
+  const RankOneSums ro = rank_one_sums(c, sh);
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
-    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * NP + i];
-    out[i] = (T)s;
+    for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+    out[i] = (T)qtilde_row(c, ro, i, s);
   }
 }
 
@@ -527,7 +553,7 @@ hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, in
 
 template <typename T>
 hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int64_t N,
-                          int kernel, double gamma, double coef0, int degree, T* norms, T* qT,
+                          int kernel, double gamma, double coef0, int degree, T* norms,
                           double* q64, double* scal, hipStream_t s) {
   constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
   const int64_t nkb = d_pad / BK;
@@ -535,15 +561,15 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
   switch (kernel) {
     case KLIN:
       hipLaunchKernelGGL((k_norms_q<T, BK, TP, KLIN>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
-                         gamma, coef0, degree, norms, qT, q64, scal);
+                         gamma, coef0, degree, norms, q64, scal);
       break;
     case KPOLY:
       hipLaunchKernelGGL((k_norms_q<T, BK, TP, KPOLY>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
-                         gamma, coef0, degree, norms, qT, q64, scal);
+                         gamma, coef0, degree, norms, q64, scal);
       break;
     default:
       hipLaunchKernelGGL((k_norms_q<T, BK, TP, KRBF>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
-                         gamma, coef0, degree, norms, qT, q64, scal);
+                         gamma, coef0, degree, norms, q64, scal);
       break;
   }
   return hipGetLastError();
@@ -594,10 +620,9 @@ hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, d
   return hipGetLastError();
 }
 
-hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                            const double* dir, double* qv, double* bpart, const double* scal,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N, dir,
+hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, int64_t N,
+                            double* qv, double* bpart, const double* scal, hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
                      qv, bpart, scal);
   return hipGetLastError();
 }
@@ -610,18 +635,18 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
   return hipGetLastError();
 }
 
-hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N,
+  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
                      rhs, r, bp_out, scal);
   return hipGetLastError();
 }
 
-hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                                 const double* rhs, double* bp_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, nslots, NP, N,
-                     rhs, bp_out);
+  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP,
+                     N, rhs, bp_out);
   return hipGetLastError();
 }
 
@@ -676,9 +701,10 @@ hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hi
 }
 
 template <typename T>
-hipError_t launch_mv_out(const double* part, int64_t nslots, int64_t NP, int64_t N, T* out,
+hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_mv_out<T>, dim3(blocks_for(N)), dim3(NT), 0, s, part, nslots, NP, N, out);
+  hipLaunchKernelGGL(k_mv_out<T>, dim3((unsigned)vec_blocks(N)), dim3(NT), 0, s, part, c, NP, N,
+                     out);
   return hipGetLastError();
 }
 
@@ -732,7 +758,7 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
   template hipError_t launch_layout<T>(const T*, int64_t, int64_t, T*, int64_t, int64_t, int*,    \
                                        hipStream_t);                                              \
   template hipError_t launch_norms_q<T>(const T*, int64_t, int64_t, int64_t, int64_t, int,        \
-                                        double, double, int, T*, T*, double*, double*,            \
+                                        double, double, int, T*, double*, double*,                \
                                         hipStream_t);                                             \
   template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
   template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
@@ -742,7 +768,7 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
                                      double, T*, hipStream_t);                                    \
   template hipError_t launch_single_point<T>(const T*, T*, double*, int*, hipStream_t);           \
   template hipError_t launch_pad_vec<T>(const T*, int64_t, T*, int64_t, hipStream_t);             \
-  template hipError_t launch_mv_out<T>(const double*, int64_t, int64_t, int64_t, T*,              \
+  template hipError_t launch_mv_out<T>(const double*, const RankOne&, int64_t, int64_t, T*,       \
                                        hipStream_t);                                              \
   template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
                                                T*, int32_t*, hipStream_t);                        \

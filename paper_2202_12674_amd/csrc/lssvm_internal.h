@@ -71,13 +71,14 @@ struct TileArgs {
   int64_t nkb;   // feature blocks of BK (even)
   const T* nA;   // squared norms of row points (RBF)
   const T* nB;   // squared norms of column points (RBF)
-  const T* qA;   // q_i = k(x_i, x_m) (symmetric mode), zero beyond N
-  const T* qB;
-  const double* pv;  // symmetric mode: the vector multiplied (fp64), zero beyond N
-  const T* wB;       // general mode: per-column weights (alpha)
-  T gamma, coef0, qmm, invC;
+  const double* pv;   // symmetric mode: the vector multiplied (fp64), zero beyond N
+  const double* q64;  // symmetric mode: q_i = k(x_i, x_m), zero beyond N
+  double* pq;         // symmetric mode: per panel I, sum p_j at [I], sum q_j p_j at [nTc + I]
+  const T* wB;        // general mode: per-column weights (alpha)
+  T gamma, coef0;
+  T rbf_scale;   // RBF exponent scale: gamma (fp64, exp) or gamma log2(e) (fp32, exp2)
   int degree;
-  int64_t nTc;   // column tiles (general mode)
+  int64_t nTc;   // column tiles (general mode); tiles per side (symmetric mode)
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // partial sums, part[slot * part_ld + row]
   const double* status;  // symmetric mode: CG status (skip the launch once done) or null
@@ -88,12 +89,25 @@ struct TileArgs {
   int64_t tile_base, ntiles;
 };
 
+// The rank-one and diagonal terms of Q~ p that the symmetric tiles leave out
+// (Eq. (13)): (Q~ p)_i = (K p)_i + (Q_mm - q_i) S - T + p_i / C for i < N,
+// with S = sum_j p_j, T = sum_j q_j p_j (summed from the diagonal tiles'
+// per-panel partials in a fixed order) and Q_mm = k(x_m, x_m) + 1/C.
+struct RankOne {
+  const double* pq;    // 2 nT panel partials: S_I, then T_I
+  int64_t nT;
+  const double* q64;   // q_i, zero beyond N
+  const double* p;     // the vector multiplied, zero beyond N
+  const double* scal;  // k(x_m, x_m) at S_KMM
+  double invC;
+};
+
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
                          int* flags, hipStream_t s);
 template <typename T>
 hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int64_t N,
-                          int kernel, double gamma, double coef0, int degree, T* norms, T* qT,
+                          int kernel, double gamma, double coef0, int degree, T* norms,
                           double* q64, double* scal, hipStream_t s);
 template <typename T>
 hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s);
@@ -106,13 +120,14 @@ hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, doubl
 // returns at once, so the host may enqueue iterations ahead of the test.
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
                                 hipStream_t s);
-hipError_t launch_cg_gather(const double* part, int64_t nslots, int64_t NP, int64_t N,
-                            const double* dir, double* qv, double* bpart, const double* scal,
-                            hipStream_t s);
+// q = Q~ dir (c.p = dir) and the block partials of dir^T q.
+hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, int64_t N,
+                            double* qv, double* bpart, const double* scal, hipStream_t s);
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s);
-hipError_t launch_cg_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+// r = rhs - Q~ x (c.p = x) and the block partials of r^T r.
+hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s);
 // Warm start: delta = r0^T r0 from the block partials, dir = r0, done if
@@ -135,7 +150,7 @@ hipError_t launch_single_point(const T* y, T* alpha_out, double* scal, int* flag
 template <typename T>
 hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hipStream_t s);
 template <typename T>
-hipError_t launch_mv_out(const double* part, int64_t nslots, int64_t NP, int64_t N, T* out,
+hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
                          hipStream_t s);
 template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
@@ -145,7 +160,7 @@ hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len
                              hipStream_t s);
 hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int slot,
                              hipStream_t s);
-hipError_t launch_true_residual(const double* part, int64_t nslots, int64_t NP, int64_t N,
+hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                                 const double* rhs, double* bp_out, hipStream_t s);
 
 // Linear-kernel decision values through w = sum_i alpha_i x_i (Eq. (15)).

@@ -63,25 +63,100 @@ template <typename T> struct TileCfg {
   static constexpr int WM = BM / 2, WN = BM / 2;
 };
 
-template <typename T> __device__ inline T texp(T x);
-template <> __device__ inline float texp<float>(float x) { return expf(x); }
-template <> __device__ inline double texp<double>(double x) { return exp(x); }
+// Exponential of the RBF kernel. fp32 uses the hardware base-2 exponential
+// (v_exp_f32) on an exponent pre-scaled by log2(e) on the host; fp64 the
+// full-precision exp.
+template <typename T> __device__ inline T rbf_exp(T x);
+template <> __device__ inline float rbf_exp<float>(float x) { return __builtin_amdgcn_exp2f(x); }
+template <> __device__ inline double rbf_exp<double>(double x) { return exp(x); }
 
-// Kernel value from the inner product g = <x_i, x_j> (and squared norms for RBF).
+// Kernel value from the inner product g = <x_i, x_j> (and squared norms for
+// RBF, with rbf_scale = gamma, times log2(e) in fp32). For the polynomial
+// kernel this returns the base gamma g + coef0; poly_power raises a whole
+// batch of bases to the degree with one uniform loop.
 template <int KER, typename T>
-__device__ inline T kernel_value(T g, T ni, T nj, T gamma, T coef0, int degree) {
+__device__ inline T kernel_value(T g, T ni, T nj, T gamma, T coef0, T rbf_scale) {
   if constexpr (KER == KLIN) {
     return g;
   } else if constexpr (KER == KPOLY) {
-    const T base = gamma * g + coef0;
-    T r = base;
-    for (int e = 1; e < degree; ++e) r *= base;
-    return r;
+    return gamma * g + coef0;
   } else {
     T dist = ni + nj - T(2) * g;
     dist = dist > T(0) ? dist : T(0);
-    return texp<T>(-gamma * dist);
+    return rbf_exp<T>(-rbf_scale * dist);
   }
+}
+
+template <typename T, int R, int C>
+__device__ inline void poly_power(T (&v)[R][C], int degree) {
+  T base[R][C];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int c = 0; c < C; ++c) base[r][c] = v[r][c];
+  for (int e = 1; e < degree; ++e)
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int c = 0; c < C; ++c) v[r][c] *= base[r][c];
+}
+
+// ------------------------------------------------------ cross-lane sums -----
+// fp64 value of another lane: a DPP permutation (gfx9 encodings) applied to
+// both 32-bit halves.
+constexpr int kDppQuadXor1 = 0xB1;       // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;       // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowRor8 = 0x128;       // lane l <- lane l ^ 8 within 16-lane rows
+constexpr int kDppRowHalfMirror = 0x141; // lane l <- lane 7 - l within 8-lane halves
+
+__device__ inline uint64_t as_u64(double v) { return __builtin_bit_cast(uint64_t, v); }
+__device__ inline double as_f64(uint32_t lo, uint32_t hi) {
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+template <int CTRL>
+__device__ inline double dpp_move(double v) {
+  const uint64_t u = as_u64(v);
+  const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+  return as_f64((uint32_t)lo, (uint32_t)hi);
+}
+
+// Sum over the 8 lanes of a half-row (lane bits 0..2), every lane receiving
+// it: the half-mirror pairs l with 7 - l, then the two quad exchanges join
+// the four pairs.
+__device__ inline double sum8(double v) {
+  v += dpp_move<kDppRowHalfMirror>(v);
+  v += dpp_move<kDppQuadXor1>(v);
+  v += dpp_move<kDppQuadXor2>(v);
+  return v;
+}
+
+// Reduce-scatter steps: from a pair (a, b) in every lane, lanes with the
+// given lane bit clear end up with a + a', lanes with it set with b + b',
+// where ' is the partner lane across that bit. Each halves the values a lane
+// carries with one exchange per pair instead of one per value.
+__device__ inline double scatter_bit3(double a, double b, bool bit3) {
+  const double keep = bit3 ? b : a, send = bit3 ? a : b;
+  return keep + dpp_move<kDppRowRor8>(send);
+}
+// bit 4: v_permlane16_swap exchanges the odd 16-lane rows of its first
+// operand with the even rows of its second
+__device__ inline double scatter_bit4(double a, double b) {
+  const uint64_t ua = as_u64(a), ub = as_u64(b);
+  const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)ua, (uint32_t)ub, false, false);
+  const auto hi =
+      __builtin_amdgcn_permlane16_swap((uint32_t)(ua >> 32), (uint32_t)(ub >> 32), false, false);
+  return as_f64(lo[0], hi[0]) + as_f64(lo[1], hi[1]);
+}
+// bit 5: v_permlane32_swap exchanges the upper 32 lanes of its first operand
+// with the lower 32 lanes of its second
+__device__ inline double scatter_bit5(double a, double b) {
+  const uint64_t ua = as_u64(a), ub = as_u64(b);
+  const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)ua, (uint32_t)ub, false, false);
+  const auto hi =
+      __builtin_amdgcn_permlane32_swap((uint32_t)(ua >> 32), (uint32_t)(ub >> 32), false, false);
+  return as_f64(lo[0], hi[0]) + as_f64(lo[1], hi[1]);
 }
 
 // t = J (J + 1) / 2 + I with 0 <= I <= J: enumerates the upper triangle of
@@ -100,13 +175,13 @@ __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // ---------------------------------------------------------- a4 tiles --------
 // One T x T tile of the pairwise contraction G = X_I X_J^T per workgroup,
-// feature blocks of BK staged global -> registers -> LDS (double-buffered)
-// and fed to the matrix cores. The epilogue turns G into kernel values and
-// then into Q~ entries (symmetric mode) and folds them into row sums
-// (times p_j) and, off the diagonal, column sums (times p_i), so that each
-// off-diagonal tile serves both triangles. Row and column sums are reduced
-// across lanes and waves in a fixed order and written as fp64 partials,
-// one slot per tile column (rows of block I) or tile row (rows of block J).
+// feature blocks of BK staged global -> LDS (double-buffered) and fed to the
+// matrix cores. The epilogue turns G into kernel values and folds them into
+// row sums (times p_j) and, off the diagonal, column sums (times p_i), so
+// that each off-diagonal tile serves both triangles. Row and column sums are
+// reduced across lanes and waves in a fixed order and written as fp64
+// partials, one slot per tile column (rows of block I) or tile row (rows of
+// block J).
 template <typename T, bool SYM, int KER>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles(
     TileArgs<T> a) {
@@ -265,77 +340,107 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     __syncthreads();
   }
 
-  // ---- epilogue: kernel values, Q~ entries, row and column sums
-  // Kernel values and Q~ entries are formed in T; products with the vector
-  // and the sums are fp64, so an fp32 product uses the fp64 CG direction as it
-  // is instead of a rounded copy.
+  // ---- epilogue: kernel values, row and column sums
+  // Symmetric mode accumulates K_IJ p_J by rows and K_IJ^T p_I by columns;
+  // the rank-one and diagonal terms that turn K into Q~ (Eq. (13)) are added
+  // by the kernels that gather the partials. Kernel values are formed in T,
+  // their products with the vector and all sums in fp64, so an fp32 product
+  // uses the fp64 CG direction as it is instead of a rounded copy.
   const bool diag = SYM && (I == J);
-  int64_t gj[CB];
-  T nBj[CB], qBj[CB];
+  T nBj[CB];
   double pBj[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
-    gj[j] = J * BM + wn * C::WN + j * MF::M + cl;
-    nBj[j] = (KER == KRBF) ? a.nB[gj[j]] : T(0);
-    qBj[j] = SYM ? a.qB[gj[j]] : T(0);
-    if constexpr (SYM) pBj[j] = a.pv[gj[j]];
-    else pBj[j] = (double)a.wB[gj[j]];
+    const int64_t gj = J * BM + wn * C::WN + j * MF::M + cl;
+    nBj[j] = (KER == KRBF) ? a.nB[gj] : T(0);
+    if constexpr (SYM) pBj[j] = a.pv[gj];
+    else pBj[j] = (double)a.wB[gj];
   }
   double cs[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) cs[j] = 0.0;
-  // one row block at a time: its row sums are reduced and parked in LDS at
-  // once, which keeps few values live next to the accumulators
-  constexpr int VH = MF::NACC > 8 ? 8 : MF::NACC;   // accumulator elements per pass
+  const bool bit3 = (lane >> 3) & 1;
+  const int bit4 = (lane >> 4) & 1;
+  // one row block and VH accumulator elements at a time: their row sums are
+  // reduced and parked in LDS at once, which keeps few values live next to
+  // the accumulators
+  constexpr int VH = MF::NACC > 8 ? 8 : MF::NACC;
+  static_assert(MF::M == 32 ? VH == 8 : (MF::M == 16 && VH == 4), "row-sum reduction layout");
+  constexpr int NTOT = MF::M == 32 ? VH / 4 : VH / 2;   // row totals per lane and pass
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
 #pragma unroll
   for (int v0 = 0; v0 < MF::NACC; v0 += VH) {
+    T kv[VH][CB];
+    double pAi[VH];
+#pragma unroll
+    for (int vv = 0; vv < VH; ++vv) {
+      const int64_t gi = I * BM + wm * C::WM + i * MF::M + MF::row(v0 + vv, lane);
+      const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
+      pAi[vv] = SYM ? a.pv[gi] : 0.0;
+#pragma unroll
+      for (int j = 0; j < CB; ++j)
+        kv[vv][j] = kernel_value<KER, T>(acc[i][j][v0 + vv], nAi, nBj[j], a.gamma, a.coef0,
+                                         a.rbf_scale);
+    }
+    if constexpr (KER == KPOLY) poly_power(kv, a.degree);
     double rs[VH];
 #pragma unroll
     for (int vv = 0; vv < VH; ++vv) {
-      const int v = v0 + vv;
-      const int lr = wm * C::WM + i * MF::M + MF::row(v, lane);
-      const int64_t gi = I * BM + lr;
-      const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
-      const T qAi = SYM ? a.qA[gi] : T(0);
-      const double pAi = SYM ? a.pv[gi] : 0.0;
       double rsum = 0.0;
 #pragma unroll
       for (int j = 0; j < CB; ++j) {
-        const T kv = kernel_value<KER, T>(acc[i][j][v], nAi, nBj[j], a.gamma, a.coef0, a.degree);
-        if constexpr (SYM) {
-          T qt = kv - qAi - qBj[j] + a.qmm;
-          if (gi == gj[j]) qt += a.invC;
-          rsum += (double)qt * pBj[j];
-          cs[j] += (double)qt * pAi;
-        } else {
-          rsum += (double)kv * pBj[j];
-        }
+        const double k = (double)kv[vv][j];
+        rsum += k * pBj[j];
+        if constexpr (SYM) cs[j] += k * pAi[vv];
       }
       rs[vv] = rsum;
     }
-    // lanes that share a row differ only in the bits of cl
+    // Row totals: the M lanes of a row differ in the bits of cl. Reduce-
+    // scatter over the high bits of cl, then a full sum over its low 3 bits;
+    // lane cl then holds the totals of elements v0 + 4s + 2 bit3 + bit4 (fp32,
+    // M = 32) or v0 + 2s + bit3 (fp64, M = 16).
+    double tot[NTOT];
+    int ve[NTOT];
+    if constexpr (MF::M == 32) {
+      double u[VH / 2];
 #pragma unroll
-    for (int vv = 0; vv < VH; ++vv)
+      for (int t = 0; t < VH / 2; ++t) u[t] = scatter_bit4(rs[2 * t], rs[2 * t + 1]);
 #pragma unroll
-      for (int off = 1; off < MF::M; off <<= 1) rs[vv] += __shfl_xor(rs[vv], off);
-    if (cl == 0) {
+      for (int t = 0; t < VH / 4; ++t) {
+        tot[t] = sum8(scatter_bit3(u[2 * t], u[2 * t + 1], bit3));
+        ve[t] = v0 + 4 * t + 2 * (int)bit3 + bit4;
+      }
+    } else {
 #pragma unroll
-      for (int vv = 0; vv < VH; ++vv)
-        red_r[wn][wm * C::WM + i * MF::M + MF::row(v0 + vv, lane)] = rs[vv];
+      for (int t = 0; t < VH / 2; ++t) {
+        tot[t] = sum8(scatter_bit3(rs[2 * t], rs[2 * t + 1], bit3));
+        ve[t] = v0 + 2 * t + (int)bit3;
+      }
+    }
+    if ((cl & 7) == 0) {
+#pragma unroll
+      for (int t = 0; t < NTOT; ++t)
+        red_r[wn][wm * C::WM + i * MF::M + MF::row(ve[t], lane)] = tot[t];
     }
   }
   }
-  // lanes that share a column differ only in the bits above cl
-#pragma unroll
-  for (int j = 0; j < CB; ++j)
-#pragma unroll
-    for (int off = MF::M; off < 64; off <<= 1) cs[j] += __shfl_xor(cs[j], off);
-
-  if (SYM && kl == 0) {
-#pragma unroll
-    for (int j = 0; j < CB; ++j) red_c[wm][wn * C::WN + j * MF::M + cl] = cs[j];
+  if constexpr (SYM) {
+    // Column totals: the lanes of a column differ in the bits above cl
+    // (bit 5 for fp32, bits 4 and 5 for fp64); after the reduce-scatter every
+    // lane holds the total of one of the wave's columns.
+    double ct;
+    int jc;
+    if constexpr (MF::M == 32) {
+      static_assert(CB == 2, "fp32 column layout");
+      ct = scatter_bit5(cs[0], cs[1]);
+      jc = lane >> 5;
+    } else {
+      static_assert(CB == 4, "fp64 column layout");
+      ct = scatter_bit4(scatter_bit5(cs[0], cs[1]), scatter_bit5(cs[2], cs[3]));
+      jc = 2 * bit4 + (lane >> 5);
+    }
+    red_c[wm][wn * C::WN + jc * MF::M + cl] = ct;
   }
   __syncthreads();
   if (tid < BM) {
@@ -349,6 +454,40 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
     for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
     a.part[I * a.part_ld + J * BM + c] = s;
+  }
+  if constexpr (SYM) {
+    // A diagonal tile also leaves its panel's share of the rank-one terms:
+    // S_I = sum p_j and T_I = sum q_j p_j over the points j of panel I.
+    if (diag) {
+      constexpr int PW = BM / 64;   // waves holding one point each per lane
+      __shared__ double red_d[PW][2];
+      double sp = 0.0, sq = 0.0;
+      if (tid < BM) {
+        const int64_t j = I * BM + tid;
+        sp = a.pv[j];
+        sq = a.q64[j] * sp;
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        sp += __shfl_xor(sp, off);
+        sq += __shfl_xor(sq, off);
+      }
+      if (lane == 0 && wave < PW) {
+        red_d[wave][0] = sp;
+        red_d[wave][1] = sq;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        double s0 = 0.0, s1 = 0.0;
+#pragma unroll
+        for (int w = 0; w < PW; ++w) {
+          s0 += red_d[w][0];
+          s1 += red_d[w][1];
+        }
+        a.pq[I] = s0;
+        a.pq[a.nTc + I] = s1;
+      }
+    }
   }
 }
 
