@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import statistics
@@ -37,12 +38,22 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def code_only(text: str) -> str:
+    """C++ source without comments, whitespace collapsed: what the compiler sees
+    of it (the kernel sources hold no string literal that contains a comment
+    marker)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the tile kernel's source (tiles.h and the shared internal header)."""
+    """Hash of the tile kernel's code (tiles.h and the shared internal header,
+    comments left out), so a measurement stays tied to the code it measured."""
     h = hashlib.sha256()
     for f in ("tiles.h", "lssvm_internal.h"):
-        with open(os.path.join(ROOT, "paper_2202_12674_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2202_12674_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

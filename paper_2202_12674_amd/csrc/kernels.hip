@@ -3,9 +3,10 @@
 // a1  k_layout        row-major points -> padded feature-blocked layout (Sec. III-A)
 // a2  k_norms_q       squared norms, q_i = k(x_i, x_m) and k(x_m, x_m) (Sec. III-C2)
 // a3  k_rhs_init      rhs = ybar - y_m 1 (Eq. (14)), CG start vectors
-// a4  k_tiles         implicit Q~ p (Eq. (16)) on the matrix cores, one tile of the
-//                     upper triangle per workgroup (Sec. III-C1), rows and columns
-//                     accumulated from the same tile
+// a4  k_tiles         implicit K p on the matrix cores, one tile of the upper
+//                     triangle per workgroup (Sec. III-C1), rows and columns
+//                     accumulated from the same tile; k_cg_gather adds the
+//                     rank-one and diagonal terms that make it Q~ p (Eqs. (13), (16))
 // a5  k_cg_*          CG vector updates with fixed-order fp64 reductions (Sec. III-B)
 // a6  k_bias          alpha_m and b (Eqs. (11), (15))
 // a7  k_tiles<gen>    decision values sum_j alpha_j k(x_j, x) + b (Eq. (10))
