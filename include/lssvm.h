@@ -214,6 +214,14 @@ const char* lssvm_last_error(void);
  * 0 for an unknown dtype. Informational: sizes need no padding by the caller. */
 int32_t lssvm_tile_size(int32_t dtype);
 
+/* Workgroups per upper-triangle tile in the implicit products of lssvm_train
+ * and lssvm_matvec for n >= 2 points of d features: 1, except for the linear
+ * kernel on problems with few tiles, whose features are split over 2..16
+ * workgroups per tile (the partial sums add up because the linear kernel
+ * value is the inner product itself) so that the tiles fill the device.
+ * 0 for arguments out of range. Informational. */
+int32_t lssvm_tile_split(int64_t n, int64_t d, int32_t dtype, int32_t kernel);
+
 #ifdef __cplusplus
 }
 #endif

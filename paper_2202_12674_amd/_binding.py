@@ -95,6 +95,8 @@ _SIGS = {
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                         ctypes.c_int64, ctypes.c_int32]),
     "lssvm_tile_size": (ctypes.c_int32, [ctypes.c_int32]),
+    "lssvm_tile_split": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                          ctypes.c_int32]),
 }
 
 

@@ -80,7 +80,40 @@ struct Geometry {
   int64_t nT;       // tiles per edge of the reduced system
   int64_t NP;       // nT * tile: padded length of every CG vector
   int64_t nb;       // blocks of the CG vector kernels over NP (block partials per reduction)
+  int64_t ksplit;   // linear kernel: workgroups per tile, each over a share of the features
 };
+
+inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
+
+// Workgroups resident at once in a tile launch: two per CU on 256 CUs.
+constexpr int64_t kResidentTiles = 512;
+#ifndef LSSVM_LINEAR_SPLIT_MAX
+#define LSSVM_LINEAR_SPLIT_MAX 16
+#endif
+
+// Feature split of the linear kernel's tiles. A product of W tiles split S
+// ways runs in ceil(W S / R) rounds of R resident workgroups, each round as
+// long as 1/S of a tile plus a fixed cost of about two feature blocks (the
+// first block's load latency and the epilogue). Small problems, whose tiles
+// fill the chip once and leave a sliver for a second round, gain most; large
+// ones keep S = 1. S halves the block count, which must stay even.
+inline int64_t linear_split(int64_t nT, int64_t nkb) {
+  const int64_t W = tri_count(nT);
+  const double f = 2.0 / (double)nkb;
+  auto cost = [&](int64_t S) {
+    return (double)((W * S + kResidentTiles - 1) / kResidentTiles) * (1.0 / (double)S + f);
+  };
+  int64_t best = 1;
+  double best_cost = cost(1);
+  for (int64_t S = 2; S <= LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0; S *= 2) {
+    const double c = cost(S);
+    if (c < 0.95 * best_cost) {   // a clear gain only: each split adds partial slots
+      best = S;
+      best_cost = c;
+    }
+  }
+  return best;
+}
 
 template <typename T>
 Geometry geometry(int64_t n, int64_t d) {
@@ -95,6 +128,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.nT = (g.N + g.tile - 1) / g.tile;
   g.NP = g.nT * g.tile;
   g.nb = vec_blocks(g.NP);
+  g.ksplit = linear_split(g.nT, g.d_pad / g.bk);
   return g;
 }
 
@@ -127,8 +161,6 @@ struct TrainWs {
   size_t bytes;
 };
 
-inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
-
 // Visit order of the upper-triangle tiles: super-tiles of GROUP x GROUP tiles,
 // column by column; inside a super-tile, column by column. Packed (I << 16) | J.
 std::vector<uint32_t> tile_order(int64_t nT, int group) {
@@ -150,7 +182,7 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.Xt = c.take<T>(g.d_pad * g.ld);
   w.norms = c.take<T>(g.ld);
   w.q64 = c.take<double>(g.ld);
-  w.part = c.take<double>(g.nT * g.NP);
+  w.part = c.take<double>(g.nT * g.ksplit * g.NP);   // slots: nT, or nT ksplit (linear)
   w.pq = c.take<double>(2 * g.nT);
   w.rhs = c.take<double>(g.NP);
   w.x = c.take<double>(g.NP);
@@ -288,8 +320,8 @@ int check_sizes(int64_t n, int64_t d, int64_t min_n) {
   if (n < min_n) return fail(LSSVM_EINVAL, "n must be >= %lld (got %lld)", (long long)min_n,
                              (long long)n);
   if (d < 1) return fail(LSSVM_EINVAL, "d must be >= 1 (got %lld)", (long long)d);
-  // the layout grid has ceil(d / 64) blocks in y (<= 65535) and the
-  // triangle of tiles must fit one 32-bit grid dimension
+  // supported range: the tile partials alone take n^2 / 16 bytes (1 TiB at
+  // n = 2^22), and the tile order packs tile indices in 16 bits
   if (n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
     return fail(LSSVM_EINVAL, "problem too large (n=%lld, d=%lld)", (long long)n, (long long)d);
   return LSSVM_OK;
@@ -310,9 +342,14 @@ template <typename T> T rbf_scale(double gamma);
 template <> float rbf_scale<float>(double gamma) { return (float)(gamma * 1.4426950408889634); }
 template <> double rbf_scale<double>(double gamma) { return gamma; }
 
+// Workgroups per symmetric tile for this kernel function.
+inline int64_t tile_split(const Geometry& g, int32_t kernel) {
+  return kernel == LSSVM_LINEAR ? g.ksplit : 1;
+}
+
 template <typename T>
 TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
-                     const double* p) {
+                     int32_t kernel, const double* p) {
   TileArgs<T> a{};
   a.A = w.Xt;
   a.B = w.Xt;
@@ -329,6 +366,7 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.rbf_scale = rbf_scale<T>(kp.gamma);
   a.degree = kp.degree;
   a.nTc = g.nT;
+  a.ksplit = tile_split(g, kernel);
   a.order = LSSVM_TILE_GROUP > 0 ? w.order : nullptr;
   a.part = w.part;
   a.part_ld = g.NP;
@@ -365,8 +403,9 @@ int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t ker
 
 // The terms of Q~ p that the tile partials leave out, for the vector p.
 template <typename T>
-RankOne rank_one(const Geometry& g, const TrainWs<T>& w, double C, const double* p) {
-  return RankOne{w.pq, g.nT, w.q64, p, w.scal, 1.0 / C};
+RankOne rank_one(const Geometry& g, const TrainWs<T>& w, int32_t kernel, double C,
+                 const double* p) {
+  return RankOne{w.pq, g.nT, g.nT * tile_split(g, kernel), w.q64, p, w.scal, 1.0 / C};
 }
 
 // One implicit product K p into the partial-sum buffer (plus the per-panel
@@ -374,8 +413,8 @@ RankOne rank_one(const Geometry& g, const TrainWs<T>& w, double C, const double*
 template <typename T>
 int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
                     int32_t kernel, const double* p, hipStream_t s) {
-  TileArgs<T> a = sym_args<T>(g, w, kp, p);
-  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT), s));
+  TileArgs<T> a = sym_args<T>(g, w, kp, kernel, p);
+  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT) * a.ksplit, s));
   return LSSVM_OK;
 }
 
@@ -383,9 +422,9 @@ template <typename T>
 int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp, int32_t kernel,
                  const double* p, hipStream_t s, MatvecTimer& tm, int64_t iter) {
   LSSVM_HIP(tm.start(s, iter));
-  TileArgs<T> a = sym_args<T>(g, w, kp, p);
+  TileArgs<T> a = sym_args<T>(g, w, kp, kernel, p);
   a.status = w.scal + S_STATUS;   // skip the launch once CG has stopped
-  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, g.nT * (g.nT + 1) / 2, s));
+  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT) * a.ksplit, s));
   LSSVM_HIP(tm.stop(s));
   return LSSVM_OK;
 }
@@ -464,7 +503,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     // set from rhs^T rhs above is kept
     LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
     LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
     LSSVM_HIP(launch_warm_start(w.bp1, g.nb, w.scal, w.r, w.dir, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
@@ -481,12 +520,12 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
       const int64_t k = ++queued;
       const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
       LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
-      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, C, w.dir), g.NP, g.N, w.qv, w.bp0, w.scal, s));
+      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv, w.bp0, w.scal, s));
       if (k % kReplaceEvery == 0) {
         LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
         LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.x, s, tm, k));
-        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
       } else {
         LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
@@ -553,7 +592,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
       double tr = 0.0;
       if (delta0 > 0.0) {
         LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, C, w.x), g.NP, g.N, w.rhs, w.bp1, s));
+        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.bp1, s));
         LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
         LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
                                  hipMemcpyDeviceToHost, s));
@@ -606,7 +645,7 @@ int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_pa
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
   LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, s));
   LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.dir, s));
-  LSSVM_HIP(launch_mv_out<T>(w.part, rank_one(g, w, C, w.dir), g.NP, g.N, out, s));
+  LSSVM_HIP(launch_mv_out<T>(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, out, s));
   LSSVM_HIP(hipStreamSynchronize(s));
   return LSSVM_OK;
 }
@@ -654,6 +693,7 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   a.rbf_scale = rbf_scale<T>(kp.gamma);
   a.degree = kp.degree;
   a.nTc = w.nTc;
+  a.ksplit = 1;
   a.part = w.part;
   a.part_ld = w.ld_te;
   LSSVM_HIP(launch_tiles_gen<T>(a, kernel, w.nTr, s));
@@ -730,6 +770,14 @@ size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32
 int32_t lssvm_tile_size(int32_t dtype) {
   if (dtype == LSSVM_F64) return TileShape<double>::T;
   if (dtype == LSSVM_F32) return TileShape<float>::T;
+  return 0;
+}
+
+int32_t lssvm_tile_split(int64_t n, int64_t d, int32_t dtype, int32_t kernel) {
+  if (n < 2 || d < 1 || n > (int64_t(1) << 22) || d > (int64_t(1) << 21)) return 0;
+  if (kernel != LSSVM_LINEAR && kernel != LSSVM_POLY && kernel != LSSVM_RBF) return 0;
+  if (dtype == LSSVM_F64) return (int32_t)tile_split(geometry<double>(n, d), kernel);
+  if (dtype == LSSVM_F32) return (int32_t)tile_split(geometry<float>(n, d), kernel);
   return 0;
 }
 

@@ -211,7 +211,7 @@ __global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ pa
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
     if (i < N) {
-      for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+      for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
       s = qtilde_row(c, ro, i, s);
     }
     qv[i] = s;
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
     double ri = 0.0;
     if (i < N) {
       double s = 0.0;
-      for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+      for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
       ri = rhs[i] - qtilde_row(c, ro, i, s);
     }
     r[i] = ri;
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
   double v = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
-    for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+    for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
     const double ri = rhs[i] - qtilde_row(c, ro, i, s);
     v += ri * ri;
   }
@@ -501,7 +501,7 @@ __global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part,
   const RankOneSums ro = rank_one_sums(c, sh);
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
     double s = 0.0;
-    for (int64_t sl = 0; sl < c.nT; ++sl) s += part[sl * NP + i];
+    for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
     out[i] = (T)qtilde_row(c, ro, i, s);
   }
 }

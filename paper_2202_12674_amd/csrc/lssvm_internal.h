@@ -79,6 +79,9 @@ struct TileArgs {
   T rbf_scale;   // RBF exponent scale: gamma (fp64, exp) or gamma log2(e) (fp32, exp2)
   int degree;
   int64_t nTc;   // column tiles (general mode); tiles per side (symmetric mode)
+  int64_t ksplit;  // symmetric linear mode: workgroups per tile, each over nkb / ksplit
+                   // feature blocks (an even count); row partials of tile (I, J) and
+                   // split s go to slot J ksplit + s, column partials to I ksplit + s
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // partial sums, part[slot * part_ld + row]
   const double* status;  // symmetric mode: CG status (skip the launch once done) or null
@@ -96,6 +99,7 @@ struct TileArgs {
 struct RankOne {
   const double* pq;    // 2 nT panel partials: S_I, then T_I
   int64_t nT;
+  int64_t nslots;      // tile partial slots to sum per row
   const double* q64;   // q_i, zero beyond N
   const double* p;     // the vector multiplied, zero beyond N
   const double* scal;  // k(x_m, x_m) at S_KMM

@@ -225,19 +225,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     if (a.status && a.status[ST_DONE] != 0.0) return;   // CG already stopped
   }
   int64_t I, J;
-  const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's tile slot
+  // Linear symmetric products may split the features of every tile over
+  // KS workgroups (each sums K p over its share; the sums add up because the
+  // kernel value is the inner product itself): workgroup slot v then takes
+  // split v % KS of tile v / KS.
+  const int64_t KS = (SYM && KER == KLIN) ? a.ksplit : 1;
+  int64_t ks = 0;
+  const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's slot
   if constexpr (SYM) {
+    int64_t v = t;
     if (a.order) {
       // workgroup w runs on XCD w % 8 (chunks start at multiples of 8, so this
       // holds for the slot t too): give each XCD a contiguous run of the order
       const int64_t G = a.ntiles;
       const int64_t x = t % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
-      const int64_t slot = x * per + (x < extra ? x : extra) + t / kNumXcd;
-      const uint32_t packed = a.order[slot];
+      v = x * per + (x < extra ? x : extra) + t / kNumXcd;
+    }
+    const int64_t tile = KS > 1 ? v / KS : v;
+    ks = KS > 1 ? v - tile * KS : 0;
+    if (a.order) {
+      const uint32_t packed = a.order[tile];
       I = packed >> 16;
       J = packed & 0xFFFFu;
     } else {
-      tri_index(t, I, J);
+      tri_index(tile, I, J);
     }
   } else {
     I = t / a.nTc;
@@ -246,9 +257,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // panel I is nkb consecutive blocks of BM * BK elements
-  const T* __restrict__ Ap = a.A + I * a.nkb * BM * BK;
-  const T* __restrict__ Bp = a.B + J * a.nkb * BM * BK;
+  // panel I is a.nkb consecutive blocks of BM * BK elements; this workgroup
+  // contracts blocks [ks nkb, (ks + 1) nkb) of it
+  const int64_t nkb = a.nkb / KS;
+  const T* __restrict__ Ap = a.A + (I * a.nkb + ks * nkb) * BM * BK;
+  const T* __restrict__ Bp = a.B + (J * a.nkb + ks * nkb) * BM * BK;
   constexpr int64_t astride = (int64_t)BM * BK, bstride = (int64_t)BM * BK;
 
   // Direct global -> LDS loads of block kb into stage buf: instruction u of
@@ -321,7 +334,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // keeping the wait behind every MFMA gains ~5% for fp64 (the other fence
   // costs each type a little).
   constexpr bool kPinLoads = sizeof(T) == 4, kPinWait = sizeof(T) == 8;
-  const int64_t nkb = a.nkb;
   dload(0, As0, Bs0);
   vm_wait_all();
   __syncthreads();
@@ -447,18 +459,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_N; ++w) s += red_r[w][tid];
-    a.part[J * a.part_ld + I * BM + tid] = s;
+    a.part[(J * KS + ks) * a.part_ld + I * BM + tid] = s;
   } else if (SYM && !diag && tid < 2 * BM) {
     const int c = tid - BM;
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
-    a.part[I * a.part_ld + J * BM + c] = s;
+    a.part[(I * KS + ks) * a.part_ld + J * BM + c] = s;
   }
   if constexpr (SYM) {
     // A diagonal tile also leaves its panel's share of the rank-one terms:
     // S_I = sum p_j and T_I = sum q_j p_j over the points j of panel I.
-    if (diag) {
+    if (diag && ks == 0) {
       constexpr int PW = BM / 64;   // waves holding one point each per lane
       __shared__ double red_d[PW][2];
       double sp = 0.0, sq = 0.0;

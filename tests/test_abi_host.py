@@ -50,6 +50,29 @@ def test_workspace_sizes():
     assert L.lssvm_tile_size(5) == 0
 
 
+def test_tile_split():
+    """The linear kernel's feature split: 1 for the other kernels and for large
+    problems, a power of two up to 16 for small ones, always leaving an even
+    number of feature blocks per workgroup; 0 outside the supported range."""
+    L = P.lib()
+    for args in [(1, 64, 0, 0), (256, 0, 0, 0), (256, 64, 9, 0), (256, 64, 0, 3),
+                 ((1 << 22) + 1, 64, 0, 0), (256, (1 << 21) + 1, 1, 0)]:
+        assert L.lssvm_tile_split(*args) == 0, args
+    for dtype in (0, 1):
+        bk = 16 if dtype == 0 else 32
+        for kernel in (1, 2):
+            for n, d in [(2, 1), (4096, 1024), (32768, 4096)]:
+                assert L.lssvm_tile_split(n, d, dtype, kernel) == 1
+        assert L.lssvm_tile_split(32768, 4096, dtype, 0) == 1
+        assert L.lssvm_tile_split(16384, 2048, dtype, 0) == 1
+        assert L.lssvm_tile_split(4096, 1024, dtype, 0) > 1
+        for n in (2, 129, 600, 1000, 2000, 4096, 6000, 8192, 12000):
+            for d in (1, 7, 64, 100, 256, 1024, 4096):
+                S = L.lssvm_tile_split(n, d, dtype, 0)
+                nkb = -(-d // (2 * bk)) * 2
+                assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, (n, d, dtype, S)
+
+
 def _train(n=10, d=3, dtype=0, kernel=0, params=None, C=1.0, eps=1e-3, max_iter=0,
            ws=ALIGNED_WS, ws_bytes=1 << 40, X=FAKE, y=FAKE, alpha=FAKE, b=True, info=None):
     L = P.lib()

@@ -107,6 +107,44 @@ def test_matvec_small_shapes(torch_dev, dtype, kernel, n, d):
     assert rel_err(out.cpu().numpy(), ref) <= TOL_MV[dtype]
 
 
+# Linear products of few tiles split each tile's features over several
+# workgroups; these shapes give every split the library uses.
+SPLIT_SHAPES = [("f64", 4096, 256, 2), ("f64", 4096, 1024, 4), ("f64", 1000, 256, 8),
+                ("f64", 600, 1024, 16), ("f32", 2000, 1024, 2), ("f32", 1000, 256, 4),
+                ("f32", 1000, 1024, 8), ("f32", 600, 1024, 16)]
+
+
+@pytest.mark.parametrize("dtype,n,d,split", SPLIT_SHAPES)
+def test_matvec_linear_feature_split(torch_dev, dtype, n, d, split):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    L = P.lib()
+    assert L.lssvm_tile_split(n, d, 0 if dtype == "f64" else 1, 0) == split
+    cfg = small_cfg("linear", dtype, n, d, C=2.0)
+    log(f"matvec split {split} {cfg.name}")
+    X, y, _, _ = data_of(cfg)
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    Xd = to_dev(torch, dev, X)
+    for seed in (7, 8):
+        p = S.probe_vector(n - 1, cfg.np_dtype, seed=seed)
+        out = P.matvec(Xd, to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
+    e = np.zeros(n - 1, dtype=cfg.np_dtype)
+    e[n // 2] = 1   # one column: the diagonal entry and the 1/C term come from one split
+    out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+    assert rel_err(out, Qt[:, n // 2]) <= TOL_MV[dtype]
+
+
+@pytest.mark.parametrize("dtype,n,d,split", [SPLIT_SHAPES[2], SPLIT_SHAPES[5]])
+def test_train_linear_feature_split(torch_dev, dtype, n, d, split):
+    torch, dev = torch_dev
+    cfg = small_cfg("linear", dtype, n, d, C=1.0)
+    X, y, Xte, _ = data_of(cfg)
+    alpha, b, iters, spread = oracle_cg_with_spread(cfg, X, y)
+    f_te = O.decision(X, alpha, b, Xte, spec_of(cfg))
+    check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
+
+
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 @pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
 def test_matvec_unit_vectors_give_columns(torch_dev, dtype, kernel):
