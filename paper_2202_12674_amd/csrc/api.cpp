@@ -81,6 +81,8 @@ struct Geometry {
   int64_t NP;       // nT * tile: padded length of every CG vector
   int64_t nb;       // blocks of the CG vector kernels over NP (block partials per reduction)
   int64_t ksplit;   // linear kernel: workgroups per tile, each over a share of the features
+  int64_t tail_q;   // other kernels: tiles of the last partial round that are split (or 0)
+  int64_t tail_split;  // ... over this many workgroups each
 };
 
 inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
@@ -115,6 +117,19 @@ inline int64_t linear_split(int64_t nT, int64_t nkb) {
   return best;
 }
 
+// The tiles beyond the last full round of resident workgroups run one per
+// CU and take about as long as a whole round. When they are at most a
+// quarter round, each is split over S (4..16) workgroups that park their
+// partial inner products, and one more launch sums them per tile and
+// finishes it: the tail then costs ~1/S of a round plus the fixup.
+inline void tail_plan(int64_t nT, int64_t nkb, int64_t* q, int64_t* split) {
+  const int64_t Q = tri_count(nT) % kResidentTiles;
+  int64_t S = 1;
+  while (S < 16 && Q * S * 2 <= kResidentTiles && nkb % (4 * S) == 0) S *= 2;
+  *q = (Q > 0 && S >= 4) ? Q : 0;
+  *split = *q > 0 ? S : 1;
+}
+
 template <typename T>
 Geometry geometry(int64_t n, int64_t d) {
   Geometry g{};
@@ -129,6 +144,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.NP = g.nT * g.tile;
   g.nb = vec_blocks(g.NP);
   g.ksplit = linear_split(g.nT, g.d_pad / g.bk);
+  tail_plan(g.nT, g.d_pad / g.bk, &g.tail_q, &g.tail_split);
   return g;
 }
 
@@ -151,6 +167,7 @@ struct TrainWs {
   T* norms;
   double* q64;
   double* part;
+  T* gpart;     // parked inner products of split tail tiles (inside the part region)
   double* pq;   // per tile panel: sum p_j, then sum q_j p_j (2 nT)
   double *rhs, *x, *r, *dir, *qv;
   double *bp0, *bp1;
@@ -182,7 +199,14 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.Xt = c.take<T>(g.d_pad * g.ld);
   w.norms = c.take<T>(g.ld);
   w.q64 = c.take<double>(g.ld);
-  w.part = c.take<double>(g.nT * g.ksplit * g.NP);   // slots: nT, or nT ksplit (linear)
+  // Tile partials: nT ksplit slots for the linear kernel's split tiles, or nT
+  // slots followed by the parked inner products of the split tail tiles.
+  const int64_t tail_elems = g.tail_q * g.tail_split * g.tile * g.tile;
+  const int64_t slot_bytes = g.nT * g.NP * (int64_t)sizeof(double);
+  const int64_t part_bytes = std::max<int64_t>(slot_bytes * g.ksplit,
+                                               slot_bytes + tail_elems * (int64_t)sizeof(T));
+  w.part = c.take<double>((part_bytes + 7) / 8);
+  w.gpart = w.part ? reinterpret_cast<T*>(reinterpret_cast<char*>(w.part) + slot_bytes) : nullptr;
   w.pq = c.take<double>(2 * g.nT);
   w.rhs = c.take<double>(g.NP);
   w.x = c.take<double>(g.NP);
@@ -408,13 +432,32 @@ RankOne rank_one(const Geometry& g, const TrainWs<T>& w, int32_t kernel, double 
   return RankOne{w.pq, g.nT, g.nT * tile_split(g, kernel), w.q64, p, w.scal, 1.0 / C};
 }
 
+// The tile launches of one product: all tiles whole (the linear kernel's
+// split tiles included), or the full rounds whole and the tail split, parked
+// and fixed up.
+template <typename T>
+hipError_t launch_product(const Geometry& g, TileArgs<T> a, int32_t kernel, T* gpart,
+                          hipStream_t s) {
+  const int64_t W = tri_count(g.nT);
+  if (a.ksplit > 1 || g.tail_q == 0)
+    return launch_tiles_sym<T>(a, kernel, kWhole, W * a.ksplit, s);
+  const int64_t F = W - g.tail_q;
+  hipError_t e = launch_tiles_sym<T>(a, kernel, kWhole, F, s);
+  if (e != hipSuccess) return e;
+  a.tile_offset = F;
+  a.ksplit = g.tail_split;
+  a.gpart = gpart;
+  e = launch_tiles_sym<T>(a, kernel, kPartial, g.tail_q * g.tail_split, s);
+  if (e != hipSuccess) return e;
+  return launch_tiles_sym<T>(a, kernel, kFixup, g.tail_q, s);
+}
+
 // One implicit product K p into the partial-sum buffer (plus the per-panel
 // sums of the rank-one terms).
 template <typename T>
 int matvec_partials(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
                     int32_t kernel, const double* p, hipStream_t s) {
-  TileArgs<T> a = sym_args<T>(g, w, kp, kernel, p);
-  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT) * a.ksplit, s));
+  LSSVM_HIP(launch_product<T>(g, sym_args<T>(g, w, kp, kernel, p), kernel, w.gpart, s));
   return LSSVM_OK;
 }
 
@@ -423,8 +466,8 @@ int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
                  const double* p, hipStream_t s, MatvecTimer& tm, int64_t iter) {
   LSSVM_HIP(tm.start(s, iter));
   TileArgs<T> a = sym_args<T>(g, w, kp, kernel, p);
-  a.status = w.scal + S_STATUS;   // skip the launch once CG has stopped
-  LSSVM_HIP(launch_tiles_sym<T>(a, kernel, tri_count(g.nT) * a.ksplit, s));
+  a.status = w.scal + S_STATUS;   // skip the launches once CG has stopped
+  LSSVM_HIP(launch_product<T>(g, a, kernel, w.gpart, s));
   LSSVM_HIP(tm.stop(s));
   return LSSVM_OK;
 }

@@ -580,16 +580,22 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
 // items one dispatch can count; a multiple of 8, so every chunk starts on XCD 0.
 constexpr int64_t kMaxTileGrid = int64_t(1) << 23;
 
-template <typename T, bool SYM>
-hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t ntiles, hipStream_t s) {
-  a.ntiles = ntiles;
-  for (int64_t base = 0; base < ntiles; base += kMaxTileGrid) {
+template <typename T, bool SYM, int PART>
+hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t nwg, hipStream_t s) {
+  a.ntiles = nwg;
+  for (int64_t base = 0; base < nwg; base += kMaxTileGrid) {
     a.tile_base = base;
-    const dim3 grid((unsigned)std::min(kMaxTileGrid, ntiles - base));
+    const dim3 grid((unsigned)std::min(kMaxTileGrid, nwg - base));
     switch (kernel) {
-      case KLIN: hipLaunchKernelGGL((k_tiles<T, SYM, KLIN>), grid, dim3(256), 0, s, a); break;
-      case KPOLY: hipLaunchKernelGGL((k_tiles<T, SYM, KPOLY>), grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((k_tiles<T, SYM, KRBF>), grid, dim3(256), 0, s, a); break;
+      case KLIN:
+        hipLaunchKernelGGL((k_tiles<T, SYM, KLIN, PART>), grid, dim3(256), 0, s, a);
+        break;
+      case KPOLY:
+        hipLaunchKernelGGL((k_tiles<T, SYM, KPOLY, PART>), grid, dim3(256), 0, s, a);
+        break;
+      default:
+        hipLaunchKernelGGL((k_tiles<T, SYM, KRBF, PART>), grid, dim3(256), 0, s, a);
+        break;
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -598,13 +604,18 @@ hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t ntiles, hipStream_t s
 }
 
 template <typename T>
-hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s) {
-  return launch_tiles<T, true>(a, kernel, ntiles_1d, s);
+hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t nwg,
+                            hipStream_t s) {
+  switch (part) {
+    case kPartial: return launch_tiles<T, true, kPartial>(a, kernel, nwg, s);
+    case kFixup: return launch_tiles<T, true, kFixup>(a, kernel, nwg, s);
+    default: return launch_tiles<T, true, kWhole>(a, kernel, nwg, s);
+  }
 }
 
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s) {
-  return launch_tiles<T, false>(a, kernel, nTr * a.nTc, s);
+  return launch_tiles<T, false, kWhole>(a, kernel, nTr * a.nTc, s);
 }
 
 template <typename T>
@@ -761,7 +772,7 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
   template hipError_t launch_norms_q<T>(const T*, int64_t, int64_t, int64_t, int64_t, int,        \
                                         double, double, int, T*, double*, double*,                \
                                         hipStream_t);                                             \
-  template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
+  template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int, int64_t, hipStream_t);    \
   template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
   template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
                                          double*, double*, int*, hipStream_t);                    \

@@ -63,6 +63,11 @@ inline int64_t vec_blocks(int64_t len) {
 // Flags raised by kernels (int32 each).
 enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
+// What a symmetric tile launch computes: whole tiles, parked feature splits
+// of tiles (their raw inner products), or the fixup that sums a tile's parked
+// splits and finishes it.
+enum TilePart : int { kWhole = 0, kPartial = 1, kFixup = 2 };
+
 template <typename T>
 struct TileArgs {
   const T* A;    // panel-major feature-blocked row points (see k_layout)
@@ -79,9 +84,13 @@ struct TileArgs {
   T rbf_scale;   // RBF exponent scale: gamma (fp64, exp) or gamma log2(e) (fp32, exp2)
   int degree;
   int64_t nTc;   // column tiles (general mode); tiles per side (symmetric mode)
-  int64_t ksplit;  // symmetric linear mode: workgroups per tile, each over nkb / ksplit
-                   // feature blocks (an even count); row partials of tile (I, J) and
-                   // split s go to slot J ksplit + s, column partials to I ksplit + s
+  int64_t ksplit;  // symmetric mode: workgroups per tile, each over nkb / ksplit feature
+                   // blocks (an even count). Linear kernel, whole tiles: row partials
+                   // of tile (I, J) and split s go to slot J ksplit + s, column
+                   // partials to I ksplit + s. Split launches park inner products in
+                   // gpart instead and a fixup launch finishes each tile.
+  int64_t tile_offset;  // symmetric mode: first tile of the launch in the visit order
+  T* gpart;             // split launches: parked inner products, ksplit 128^2 per tile
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // partial sums, part[slot * part_ld + row]
   const double* status;  // symmetric mode: CG status (skip the launch once done) or null
@@ -114,7 +123,10 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
                           int kernel, double gamma, double coef0, int degree, T* norms,
                           double* q64, double* scal, hipStream_t s);
 template <typename T>
-hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int64_t ntiles_1d, hipStream_t s);
+// Symmetric tile launch of nwg workgroups doing `part` (a TilePart; a fixup
+// launch has one workgroup per tile).
+hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t nwg,
+                            hipStream_t s);
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
 template <typename T>

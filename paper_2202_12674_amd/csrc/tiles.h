@@ -182,7 +182,12 @@ __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // reduced across lanes and waves in a fixed order and written as fp64
 // partials, one slot per tile column (rows of block I) or tile row (rows of
 // block J).
-template <typename T, bool SYM, int KER>
+//
+// PART splits a symmetric tile's features over a.ksplit workgroups without
+// separate partial slots: kPartial workgroups park their raw inner products
+// G (the accumulators) in a.gpart and stop; a kFixup launch, one workgroup
+// per tile, sums the parked splits in split order and runs the epilogue.
+template <typename T, bool SYM, int KER, int PART>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles(
     TileArgs<T> a) {
   using MF = Mfma<T>;
@@ -225,24 +230,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     if (a.status && a.status[ST_DONE] != 0.0) return;   // CG already stopped
   }
   int64_t I, J;
-  // Linear symmetric products may split the features of every tile over
-  // KS workgroups (each sums K p over its share; the sums add up because the
-  // kernel value is the inner product itself): workgroup slot v then takes
-  // split v % KS of tile v / KS.
-  const int64_t KS = (SYM && KER == KLIN) ? a.ksplit : 1;
-  int64_t ks = 0;
+  // Symmetric tiles may have their features split over KS workgroups. For
+  // the linear kernel each split sums K p over its share into slots of its
+  // own (the sums add up because the kernel value is the inner product
+  // itself); otherwise the splits meet in the kFixup launch. Workgroup slot v
+  // takes split v % KS of tile v / KS of this launch, which starts at
+  // a.tile_offset of the visit order.
+  const int64_t KS = (SYM && (KER == KLIN || PART != kWhole)) ? a.ksplit : 1;
+  const int64_t SS = PART == kWhole ? KS : 1;   // partial slots per tile row / column
+  int64_t ks = 0, trel = 0;
   const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's slot
   if constexpr (SYM) {
     int64_t v = t;
-    if (a.order) {
+    if (a.order && PART != kFixup) {
       // workgroup w runs on XCD w % 8 (chunks start at multiples of 8, so this
       // holds for the slot t too): give each XCD a contiguous run of the order
       const int64_t G = a.ntiles;
       const int64_t x = t % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
       v = x * per + (x < extra ? x : extra) + t / kNumXcd;
     }
-    const int64_t tile = KS > 1 ? v / KS : v;
-    ks = KS > 1 ? v - tile * KS : 0;
+    trel = v;
+    if (PART != kFixup && KS > 1) {
+      trel = v / KS;
+      ks = v - trel * KS;
+    }
+    const int64_t tile = a.tile_offset + trel;
     if (a.order) {
       const uint32_t packed = a.order[tile];
       I = packed >> 16;
@@ -334,6 +346,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // keeping the wait behind every MFMA gains ~5% for fp64 (the other fence
   // costs each type a little).
   constexpr bool kPinLoads = sizeof(T) == 4, kPinWait = sizeof(T) == 8;
+  if constexpr (PART != kFixup) {
   dload(0, As0, Bs0);
   vm_wait_all();
   __syncthreads();
@@ -350,6 +363,48 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     if constexpr (kPinWait) __builtin_amdgcn_sched_barrier(0);
     vm_wait_all();
     __syncthreads();
+  }
+  }
+
+  // Split tiles: park this split's inner products, or sum all splits of the
+  // tile in split order (the same sum whichever split finished last). Thread
+  // tid's accumulators go to 16-byte units ((trel KS + s) NU + u) 256 + tid,
+  // so every store and load instruction covers 4 KiB contiguously.
+  if constexpr (PART != kWhole) {
+    constexpr int PER = 16 / (int)sizeof(T);            // elements per 16-byte unit
+    constexpr int UPB = MF::NACC / PER;                 // units per accumulator block
+    constexpr int NU = RB * CB * UPB;                   // units per thread
+    typedef T unit_t __attribute__((ext_vector_type(PER)));
+    auto unit_ptr = [&](int64_t s, int u) {
+      return reinterpret_cast<unit_t*>(a.gpart) + ((trel * KS + s) * NU + u) * 256 + tid;
+    };
+    if constexpr (PART == kPartial) {
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j)
+#pragma unroll
+          for (int w = 0; w < UPB; ++w) {
+            unit_t x;
+#pragma unroll
+            for (int e = 0; e < PER; ++e) x[e] = acc[i][j][w * PER + e];
+            *unit_ptr(ks, (i * CB + j) * UPB + w) = x;
+          }
+      return;
+    } else {
+      for (int64_t s2 = 0; s2 < KS; ++s2) {
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+          for (int j = 0; j < CB; ++j)
+#pragma unroll
+            for (int w = 0; w < UPB; ++w) {
+              const unit_t x = *unit_ptr(s2, (i * CB + j) * UPB + w);
+#pragma unroll
+              for (int e = 0; e < PER; ++e) acc[i][j][w * PER + e] += x[e];
+            }
+      }
+    }
   }
 
   // ---- epilogue: kernel values, row and column sums
@@ -459,13 +514,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_N; ++w) s += red_r[w][tid];
-    a.part[(J * KS + ks) * a.part_ld + I * BM + tid] = s;
+    a.part[(J * SS + ks) * a.part_ld + I * BM + tid] = s;
   } else if (SYM && !diag && tid < 2 * BM) {
     const int c = tid - BM;
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
-    a.part[(I * KS + ks) * a.part_ld + J * BM + c] = s;
+    a.part[(I * SS + ks) * a.part_ld + J * BM + c] = s;
   }
   if constexpr (SYM) {
     // A diagonal tile also leaves its panel's share of the rank-one terms:

@@ -145,6 +145,63 @@ def test_train_linear_feature_split(torch_dev, dtype, n, d, split):
     check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
 
 
+def tail_plan(n, d, dtype):
+    """(tail tiles, splits) of a symmetric product as the library plans it: the
+    tiles after the last full round of 512 workgroups, split 4..16 ways when
+    they are at most a quarter round."""
+    bk = 16 if dtype == "f64" else 32
+    nkb = -(-d // (2 * bk)) * 2
+    nT = -(-(n - 1) // 128)
+    Q = nT * (nT + 1) // 2 % 512
+    S = 1
+    while S < 16 and Q * S * 2 <= 512 and nkb % (4 * S) == 0:
+        S *= 2
+    return (Q, S) if Q > 0 and S >= 4 else (0, 1)
+
+
+# Tiles beyond the last full round are split over several workgroups whose
+# inner products a fixup launch sums: every tile in the tail (600 points), one
+# full round plus 16 tail tiles (4096 points), a linear product without the
+# feature split (12288 points).
+TAIL_SHAPES = [("f64", "rbf", 600, 256, (15, 8)), ("f32", "poly", 600, 256, (15, 4)),
+               ("f64", "poly", 4096, 256, (16, 8)), ("f32", "rbf", 4096, 512, (16, 8)),
+               ("f64", "linear", 12288, 1024, (48, 8))]
+
+
+@pytest.mark.parametrize("dtype,kernel,n,d,plan", TAIL_SHAPES)
+def test_matvec_tail_split(torch_dev, dtype, kernel, n, d, plan):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    assert tail_plan(n, d, dtype) == plan
+    if kernel == "linear":
+        assert P.lib().lssvm_tile_split(n, d, 0 if dtype == "f64" else 1, 0) == 1
+    cfg = small_cfg(kernel, dtype, n, d, C=2.0)
+    log(f"matvec tail {plan} {cfg.name}")
+    X, y, _, _ = data_of(cfg)
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    Xd = to_dev(torch, dev, X)
+    for seed in (7, 8):
+        p = S.probe_vector(n - 1, cfg.np_dtype, seed=seed)
+        out = P.matvec(Xd, to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
+    for j in (0, n - 2):   # columns of the first and the last tile of the visit order
+        e = np.zeros(n - 1, dtype=cfg.np_dtype)
+        e[j] = 1
+        out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt[:, j]) <= TOL_MV[dtype], j
+    del Qt
+
+
+@pytest.mark.parametrize("dtype,kernel,n,d,plan", [TAIL_SHAPES[2], TAIL_SHAPES[3]])
+def test_train_tail_split(torch_dev, dtype, kernel, n, d, plan):
+    torch, dev = torch_dev
+    cfg = small_cfg(kernel, dtype, n, d, C=1.0)
+    X, y, Xte, _ = data_of(cfg)
+    alpha, b, iters, spread = oracle_cg_with_spread(cfg, X, y)
+    f_te = O.decision(X, alpha, b, Xte, spec_of(cfg))
+    check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
+
+
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 @pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
 def test_matvec_unit_vectors_give_columns(torch_dev, dtype, kernel):
