@@ -58,8 +58,9 @@ def kernel_source_hash() -> str:
 
 
 def traffic_record(workload: str):
-    """HBM bytes per tile-kernel launch from committed rocprofv3 counter runs,
-    or None when missing or taken on a different kernel source."""
+    """HBM bytes per implicit product (its tile launches together) from
+    committed rocprofv3 counter runs, or None when missing or taken on a
+    different kernel source."""
     path = os.path.join(ROOT, "profiles", f"k_tiles_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -67,7 +68,7 @@ def traffic_record(workload: str):
         rec = json.load(fh)
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("hbm_bytes_per_product")
 
 
 def cpu_baseline(cfg, X, budget_s: float):
