@@ -169,6 +169,9 @@ __device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
   I = t - j * (j + 1) / 2;
 }
 
+// Tile rows per band of the general-mode visit order.
+constexpr int64_t kBandRows = 8;
+
 // Wait until all of this wave's vector memory operations (including direct
 // global -> LDS loads) have completed: s_waitcnt vmcnt(0), other counters free.
 __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -263,8 +266,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       tri_index(tile, I, J);
     }
   } else {
-    I = t / a.nTc;
-    J = t % a.nTc;
+    // Each XCD takes a contiguous run of slots (as above), and the slots walk
+    // bands of up to 8 tile rows column by column, so the ~64 workgroups
+    // resident on one XCD cover about 8 row panels x 8 column panels and
+    // share both in its L2.
+    const int64_t G = a.ntiles, nTr = G / a.nTc;
+    const int64_t x = t % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
+    const int64_t v = x * per + (x < extra ? x : extra) + t / kNumXcd;
+    const int64_t band = v / (kBandRows * a.nTc), r = v - band * kBandRows * a.nTc;
+    const int64_t rows = nTr - band * kBandRows < kBandRows ? nTr - band * kBandRows : kBandRows;
+    J = r / rows;
+    I = band * kBandRows + (r - J * rows);
   }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;

@@ -385,9 +385,10 @@ def test_train_configs(torch_dev, name):
 
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 @pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
-@pytest.mark.parametrize("n,nt,d", [(1, 5, 3), (300, 1, 9), (517, 300, 70)])
+@pytest.mark.parametrize("n,nt,d", [(1, 5, 3), (300, 1, 9), (517, 300, 70), (700, 1100, 40)])
 def test_predict_oracle_model(torch_dev, dtype, kernel, n, nt, d):
-    """GPU scores for the oracle's own model equal the oracle's scores."""
+    """GPU scores for the oracle's own model equal the oracle's scores. 1100 test
+    points are 9 tile rows: a full band of 8 and a band of 1 in the visit order."""
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
     cfg = small_cfg(kernel, dtype, n, d)
