@@ -265,16 +265,22 @@ def test_matvec_full_configs_golden(torch_dev, name):
     assert np.abs(out[rows] - sampled).max() / scale <= TOL_MV[cfg.dtype]
 
 
-def test_matvec_deterministic(torch_dev):
+@pytest.mark.parametrize("kernel,dtype,n,d", [("rbf", "f32", 1000, 300),      # whole tiles
+                                              ("linear", "f64", 4096, 1024),   # feature split
+                                              ("rbf", "f64", 4096, 256)])      # split tail
+def test_matvec_deterministic(torch_dev, kernel, dtype, n, d):
+    """Bitwise equal products run to run: fixed-order sums, no atomics, on every
+    way a product is split over workgroups."""
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
-    cfg = small_cfg("rbf", "f32", 1000, 300)
+    cfg = small_cfg(kernel, dtype, n, d)
     X, _, _, _ = data_of(cfg)
     Xd = to_dev(torch, dev, X)
-    p = to_dev(torch, dev, S.probe_vector(999, np.float32))
+    p = to_dev(torch, dev, S.probe_vector(n - 1, cfg.np_dtype))
     a = P.matvec(Xd, p, C=1.0, **kw_of(cfg)).cpu().numpy()
-    b = P.matvec(Xd, p, C=1.0, **kw_of(cfg)).cpu().numpy()
-    assert np.array_equal(a, b)
+    for _ in range(2):
+        b = P.matvec(Xd, p, C=1.0, **kw_of(cfg)).cpu().numpy()
+        assert np.array_equal(a, b)
 
 
 # ------------------------------------------------------------- train --------
