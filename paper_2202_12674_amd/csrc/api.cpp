@@ -142,7 +142,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.d_pad = round_up(d, 2 * g.bk);   // an even number of feature blocks (two LDS stages)
   g.nT = (g.N + g.tile - 1) / g.tile;
   g.NP = g.nT * g.tile;
-  g.nb = vec_blocks(g.NP);
+  g.nb = cg_blocks(g.NP);
   g.ksplit = linear_split(g.nT, g.d_pad / g.bk);
   tail_plan(g.nT, g.d_pad / g.bk, &g.tail_q, &g.tail_split);
   return g;

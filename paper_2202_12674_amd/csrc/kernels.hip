@@ -81,6 +81,27 @@ __device__ inline double qtilde_row(const RankOne& c, const RankOneSums& r, int6
   return kp + (r.qmm - c.q64[i]) * r.S - r.Tq + c.p[i] * c.invC;
 }
 
+// Tile partial sums of rows [r0, r0 + 32): thread (g, r) = (tid / 32, tid % 32)
+// adds slots g, g + 8, g + 16, ... of row r0 + r, then the eight group sums
+// are added in group order through sh (8 x 32 doubles). The total of row
+// r0 + tid lands in threads tid < 32. Fixed order: the same sum every run.
+// Called by every thread of the block.
+__device__ inline double row_slot_sum(const double* __restrict__ part, int64_t nslots, int64_t NP,
+                                      int64_t r0, double* sh) {
+  const int r = threadIdx.x % kRowsPerBlock, g = threadIdx.x / kRowsPerBlock;
+  const int64_t i = r0 + r;
+  double s = 0.0;
+  if (i < NP)
+    for (int64_t sl = g; sl < nslots; sl += kSlotGroups) s += part[sl * NP + i];
+  __syncthreads();   // the previous chunk's reads of sh are done
+  sh[g * kRowsPerBlock + r] = s;
+  __syncthreads();
+  double t = 0.0;
+  if (g == 0)
+    for (int k = 0; k < kSlotGroups; ++k) t += sh[k * kRowsPerBlock + r];
+  return t;
+}
+
 // ------------------------------------------------------------- a1 layout ----
 // Panel-major, feature-blocked layout. Points are grouped in panels of TP
 // (the tile edge) and features in blocks of BK; panel pb holds its nkb blocks
@@ -205,17 +226,19 @@ __global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ pa
                                                    int64_t NP, int64_t N, double* qv,
                                                    double* bpart, const double* scal) {
   __shared__ double sh[NT / 64];
+  __shared__ double rs[NT];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const RankOneSums ro = rank_one_sums(c, sh);
   double prod = 0.0;
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
-    double s = 0.0;
-    if (i < N) {
-      for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
-      s = qtilde_row(c, ro, i, s);
+  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
+       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
+    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
+    const int64_t i = r0 + threadIdx.x;
+    if (threadIdx.x < kRowsPerBlock && i < NP) {
+      const double q = i < N ? qtilde_row(c, ro, i, t) : 0.0;
+      qv[i] = q;
+      prod += c.p[i] * q;
     }
-    qv[i] = s;
-    prod += c.p[i] * s;
   }
   const double t = block_sum(prod, sh);
   if (threadIdx.x == 0) bpart[blockIdx.x] = t;
@@ -268,16 +291,16 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
                                                      const double* __restrict__ rhs, double* r,
                                                      double* bp_out, const double* scal) {
   __shared__ double sh[NT / 64];
+  __shared__ double rs[NT];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const RankOneSums ro = rank_one_sums(c, sh);
   double v = 0.0;
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
-    double ri = 0.0;
-    if (i < N) {
-      double s = 0.0;
-      for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
-      ri = rhs[i] - qtilde_row(c, ro, i, s);
-    }
+  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
+       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
+    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
+    const int64_t i = r0 + threadIdx.x;
+    if (threadIdx.x >= kRowsPerBlock || i >= NP) continue;
+    const double ri = i < N ? rhs[i] - qtilde_row(c, ro, i, t) : 0.0;
     r[i] = ri;
     v += ri * ri;
   }
@@ -291,12 +314,15 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
                                                        const double* __restrict__ rhs,
                                                        double* bp_out) {
   __shared__ double sh[NT / 64];
+  __shared__ double rs[NT];
   const RankOneSums ro = rank_one_sums(c, sh);
   double v = 0.0;
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
-    double s = 0.0;
-    for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
-    const double ri = rhs[i] - qtilde_row(c, ro, i, s);
+  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
+       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
+    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
+    const int64_t i = r0 + threadIdx.x;
+    if (threadIdx.x >= kRowsPerBlock || i >= N) continue;
+    const double ri = rhs[i] - qtilde_row(c, ro, i, t);
     v += ri * ri;
   }
   const double t = block_sum(v, sh);
@@ -498,11 +524,13 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part, RankOne c,
                                                 int64_t NP, int64_t N, T* __restrict__ out) {
   __shared__ double sh[NT / 64];
+  __shared__ double rs[NT];
   const RankOneSums ro = rank_one_sums(c, sh);
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < N; i += (int64_t)gridDim.x * NT) {
-    double s = 0.0;
-    for (int64_t sl = 0; sl < c.nslots; ++sl) s += part[sl * NP + i];
-    out[i] = (T)qtilde_row(c, ro, i, s);
+  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
+       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
+    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
+    const int64_t i = r0 + threadIdx.x;
+    if (threadIdx.x < kRowsPerBlock && i < N) out[i] = (T)qtilde_row(c, ro, i, t);
   }
 }
 
@@ -621,7 +649,7 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
                            double* dir, double* bpart, int* flags, hipStream_t s) {
-  hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
+  hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
                      dir, bpart, flags);
   return hipGetLastError();
 }
@@ -634,7 +662,7 @@ hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, d
 
 hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, int64_t N,
                             double* qv, double* bpart, const double* scal, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
+  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
                      qv, bpart, scal);
   return hipGetLastError();
 }
@@ -642,7 +670,7 @@ hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, in
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
+  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
                      par, dir, qv, x, r, bp_out, NP);
   return hipGetLastError();
 }
@@ -650,14 +678,14 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                               const double* rhs, double* r, double* bp_out, const double* scal,
                               hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
+  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
                      rhs, r, bp_out, scal);
   return hipGetLastError();
 }
 
 hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
                                 const double* rhs, double* bp_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, part, c, NP,
+  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP,
                      N, rhs, bp_out);
   return hipGetLastError();
 }
@@ -665,14 +693,14 @@ hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
                                double* hist, int64_t hist_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
+  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
                      iter, r, dir, NP, hist, hist_cap);
   return hipGetLastError();
 }
 
 hipError_t launch_warm_start(const double* bp_in, int64_t nb, double* scal, const double* r,
                              double* dir, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_warm_start, dim3((unsigned)vec_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal,
+  hipLaunchKernelGGL(k_warm_start, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal,
                      r, dir, NP);
   return hipGetLastError();
 }
@@ -715,7 +743,7 @@ hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hi
 template <typename T>
 hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_mv_out<T>, dim3((unsigned)vec_blocks(N)), dim3(NT), 0, s, part, c, NP, N,
+  hipLaunchKernelGGL(k_mv_out<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
                      out);
   return hipGetLastError();
 }

@@ -60,6 +60,16 @@ inline int64_t vec_blocks(int64_t len) {
   return b < kVecBlocks ? (b > 0 ? b : 1) : kVecBlocks;
 }
 
+// The training's CG vector kernels run one block per 32 rows of the padded
+// vectors (the gather sums each row's tile partial slots with 8 thread
+// groups, so many loads are in flight even for short vectors), at most
+// kVecBlocks, striding beyond that.
+constexpr int64_t kSlotGroups = 8, kRowsPerBlock = 256 / kSlotGroups;
+inline int64_t cg_blocks(int64_t NP) {
+  const int64_t b = NP / kRowsPerBlock;
+  return b < kVecBlocks ? (b > 0 ? b : 1) : kVecBlocks;
+}
+
 // Flags raised by kernels (int32 each).
 enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
