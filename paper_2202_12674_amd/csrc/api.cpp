@@ -546,7 +546,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     // set from rhs^T rhs above is kept
     LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
     LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
+                                 w.r, w.bp1, w.scal, s));
     LSSVM_HIP(launch_warm_start(w.bp1, g.nb, w.scal, w.r, w.dir, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
@@ -557,18 +558,26 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     if (!std::isfinite(delta))
       return fail(LSSVM_ENONFINITE, "the warm-start alpha gives a non-finite residual");
   }
+  // Iterations queued after the stop return at once but still pay for their
+  // launches, so once two status reads give a rate of decrease of r^T r, a
+  // batch is also capped at the iterations that rate needs to reach the stop
+  // threshold (with a quarter to spare).
+  int64_t it_prev = 0, need = max_iter;
+  double delta_prev = delta;
   while (!done && queued < max_iter) {
-    const int64_t nq = std::min<int64_t>(batch, max_iter - queued);
+    const int64_t nq = std::min<int64_t>(std::min(batch, need), max_iter - queued);
     for (int64_t b = 0; b < nq; ++b) {
       const int64_t k = ++queued;
       const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
       LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
-      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv, w.bp0, w.scal, s));
+      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv,
+                                 w.bp0, w.scal, s));
       if (k % kReplaceEvery == 0) {
         LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
         LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.x, s, tm, k));
-        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.r, w.bp1, w.scal, s));
+        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
+                                     w.r, w.bp1, w.scal, s));
       } else {
         LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
@@ -595,6 +604,14 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
                    (long long)it, delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0,
                    ms_since(t1));
     batch = std::min<int64_t>(2 * batch, 32);
+    need = max_iter;
+    if (it > it_prev && delta > 0.0 && delta < delta_prev && st[ST_STOP] < delta) {
+      const double per_it = std::log(delta / delta_prev) / (double)(it - it_prev);   // < 0
+      const double to_go = std::log(st[ST_STOP] / delta) / per_it;                    // > 0
+      if (to_go < 1e9) need = std::max<int64_t>(1, (int64_t)std::ceil(1.25 * to_go));
+    }
+    it_prev = it;
+    delta_prev = delta;
   }
   const bool converged = done && !broke;
   const int64_t nmv = it + it / kReplaceEvery + warm_products;
@@ -635,7 +652,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
       double tr = 0.0;
       if (delta0 > 0.0) {
         LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.bp1, s));
+        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N,
+                                       w.rhs, w.bp1, s));
         LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
         LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
                                  hipMemcpyDeviceToHost, s));

@@ -625,7 +625,8 @@ int read_model(const char* path, T* X, T* alpha, T* y, int64_t n, int64_t d, int
 // ------------------------------------------------------------------- checks --
 
 int check_dims(int64_t n, int64_t d, bool allow_empty) {
-  if (n < (allow_empty ? 0 : 1)) return fail(LSSVM_EINVAL, "n must be >= 1 (got %lld)", (long long)n);
+  if (n < (allow_empty ? 0 : 1))
+    return fail(LSSVM_EINVAL, "n must be >= 1 (got %lld)", (long long)n);
   if (d < 0 || d > kMaxDim) return fail(LSSVM_EINVAL, "d out of range (got %lld)", (long long)d);
   if (n > 0 && d > 0 && n > std::numeric_limits<int64_t>::max() / d)
     return fail(LSSVM_EINVAL, "n * d overflows");

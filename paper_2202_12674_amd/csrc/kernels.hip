@@ -649,8 +649,8 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
                            double* dir, double* bpart, int* flags, hipStream_t s) {
-  hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs, x, r,
-                     dir, bpart, flags);
+  hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs,
+                     x, r, dir, bpart, flags);
   return hipGetLastError();
 }
 
@@ -670,8 +670,8 @@ hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, in
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, x_only, bp_in, nb, scal,
-                     par, dir, qv, x, r, bp_out, NP);
+  hipLaunchKernelGGL(k_cg_update, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, x_only, bp_in,
+                     nb, scal, par, dir, qv, x, r, bp_out, NP);
   return hipGetLastError();
 }
 
@@ -693,8 +693,8 @@ hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
                                double* hist, int64_t hist_cap, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal, par,
-                     iter, r, dir, NP, hist, hist_cap);
+  hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb,
+                     scal, par, iter, r, dir, NP, hist, hist_cap);
   return hipGetLastError();
 }
 

@@ -27,7 +27,8 @@ constexpr int kProbeBlocks = 2 * 256;
 constexpr int kProbeThreads = 256;
 constexpr int kProbeIters = 32768;
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_loop_f32(int iters, float seed, float* sink) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_loop_f32(
+    int iters, float seed, float* sink) {
   floatx16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
   const float a = seed * (float)(threadIdx.x & 7), b = seed;
   for (int k = 0; k < iters; ++k) {
@@ -42,7 +43,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   sink[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_loop_f64(int iters, double seed, double* sink) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_loop_f64(
+    int iters, double seed, double* sink) {
   doublex4 c0 = {}, c1 = {}, c2 = {}, c3 = {};
   const double a = seed * (double)(threadIdx.x & 7), b = seed;
   for (int k = 0; k < iters; ++k) {

@@ -1,6 +1,7 @@
 // The a4 / a7 tile kernel: the kernel-matrix part K p of the implicit Q~
 // product (Eqs. (13), (16)) and the decision values on the gfx950 matrix
-// cores, one 128 x 128 tile of points per workgroup. Included by kernels.hip (one translation unit); kept on its own
+// cores, one 128 x 128 tile of points per workgroup. Included by kernels.hip
+// (one translation unit); kept on its own
 // so that the tile kernel's source can be identified apart from the rest.
 #pragma once
 
