@@ -202,6 +202,72 @@ def test_train_tail_split(torch_dev, dtype, kernel, n, d, plan):
     check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
 
 
+def _random_cases(count=24, seed=2026):
+    """Seeded shapes across kernels and precisions: ragged n and d that land on
+    every way a product is laid out (padding, feature splits, split tails)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for k in range(count):
+        n, d = int(rng.integers(2, 3000)), int(rng.integers(1, 700))
+        C = float(rng.choice([0.1, 1.0, 10.0]))
+        cases.append((["linear", "poly", "rbf"][k % 3], ["f64", "f32"][(k // 3) % 2], n, d, C))
+    return cases
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d,C", _random_cases())
+def test_matvec_random_shapes(torch_dev, kernel, dtype, n, d, C):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=C)
+    log(f"matvec random {cfg.name} C={C}")
+    X, y, _, _ = data_of(cfg)
+    p = S.probe_vector(n - 1, cfg.np_dtype, seed=n)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=C, **kw_of(cfg))
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), C)
+    assert rel_err(out.cpu().numpy(), Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
+
+
+def fp32_sensitivity(X, cfg):
+    """kappa(Q~) u32, a first-order bound on how far rounding the kernel values
+    to fp32 can move the solution relative to its size: lambda_min(Q~) >= 1/C
+    (Q~ = P^T Q P with P^T P >= I) and lambda_max(Q~) from power iteration."""
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
+    v = np.random.default_rng(0).standard_normal(Qt.shape[0])
+    for _ in range(30):
+        v = Qt @ v
+        v /= np.linalg.norm(v)
+    return float(v @ (Qt @ v)) * cfg.C * 2.0 ** -24
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d,C", [_random_cases()[k] for k in (0, 4, 8, 13, 17, 21)])
+def test_train_random_shapes(torch_dev, kernel, dtype, n, d, C):
+    """The full alpha / b bar where fp32 can resolve the solution to it
+    (kappa u32 <= 1e-2); for fp32 systems conditioned beyond that, two solves
+    that both meet eps may differ by up to kappa u32 in alpha, so the check is
+    what fp32 CG promises: convergence, the true residual and the test labels
+    away from near-ties."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=C)
+    X, y, Xte, _ = data_of(cfg)
+    alpha, b, iters, spread = oracle_cg_with_spread(cfg, X, y)
+    f_te = O.decision(X, alpha, b, Xte, spec_of(cfg))
+    sens = fp32_sensitivity(X, cfg) if dtype == "f32" else 0.0
+    log(f"  {cfg.name} C={C}: kappa u32 <= {sens:.1e}")
+    if sens <= 1e-2:
+        check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
+        return
+    res = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=cfg.C, eps=cfg.eps,
+                  true_residual=True, **kw_of(cfg))
+    assert res.converged and res.true_rel_residual <= 2 * cfg.eps
+    scores, labels = P.predict(to_dev(torch, dev, X), res.alpha, res.b, to_dev(torch, dev, Xte),
+                               **kw_of(cfg))
+    bad, ties = labels_match(labels.cpu().numpy(), f_te, min(1.0, 10 * sens))
+    log(f"  fp32, ill-conditioned: it {res.iterations}, true residual {res.true_rel_residual:.2e},"
+        f" {bad} label mismatches outside {ties} near-ties")
+    assert bad == 0
+
+
 @pytest.mark.parametrize("dtype", ["f64", "f32"])
 @pytest.mark.parametrize("kernel", ["linear", "poly", "rbf"])
 def test_matvec_unit_vectors_give_columns(torch_dev, dtype, kernel):
