@@ -271,13 +271,22 @@ struct HostScratch {
 };
 thread_local HostScratch g_host;
 
+// Timing events, created once per thread and device and reused by every later
+// training there (creating a few hundred events costs more than a small
+// training takes).
+struct EventPool {
+  int device = -1;
+  std::vector<hipEvent_t> ev;
+};
+thread_local EventPool g_events;
+
 // HIP events around each implicit product, recorded on the launch stream.
 // Pairs carry the CG iteration they belong to, so products that ran after
 // the stop (and returned at once) are left out.
 struct MatvecTimer {
   static constexpr int kPairs = 2 * 64;   // up to two products per queued iteration
   bool on = false;
-  hipEvent_t ev[2 * kPairs] = {};
+  hipEvent_t* ev = nullptr;   // 2 kPairs events of the thread's pool
   int64_t tag[kPairs] = {};
   int used = 0;          // event pairs recorded since the last harvest
   double total_ms = 0.0;
@@ -285,15 +294,21 @@ struct MatvecTimer {
   hipError_t init(bool enable) {
     on = enable;
     if (!on) return hipSuccess;
-    for (auto& e : ev) {
-      hipError_t r = hipEventCreate(&e);
-      if (r != hipSuccess) return r;
+    int device = 0;
+    hipError_t r = hipGetDevice(&device);
+    if (r != hipSuccess) return r;
+    if (g_events.device != device) {
+      for (hipEvent_t e : g_events.ev) (void)hipEventDestroy(e);
+      g_events.ev.clear();
+      g_events.device = device;
     }
+    while (g_events.ev.size() < (size_t)(2 * kPairs)) {
+      hipEvent_t e = nullptr;
+      if ((r = hipEventCreate(&e)) != hipSuccess) return r;
+      g_events.ev.push_back(e);
+    }
+    ev = g_events.ev.data();
     return hipSuccess;
-  }
-  ~MatvecTimer() {
-    for (auto& e : ev)
-      if (e) (void)hipEventDestroy(e);
   }
   // A batch queues at most 32 iterations of at most two products each, so the
   // pairs never run out; should they, the extra products are simply not timed.
