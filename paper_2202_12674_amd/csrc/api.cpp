@@ -178,19 +178,6 @@ struct TrainWs {
   size_t bytes;
 };
 
-// Visit order of the upper-triangle tiles: super-tiles of GROUP x GROUP tiles,
-// column by column; inside a super-tile, column by column. Packed (I << 16) | J.
-std::vector<uint32_t> tile_order(int64_t nT, int group) {
-  std::vector<uint32_t> v;
-  v.reserve((size_t)tri_count(nT));
-  const int64_t g = group > 0 ? group : nT;
-  for (int64_t sj = 0; sj < nT; sj += g)
-    for (int64_t si = 0; si <= sj; si += g)
-      for (int64_t j = sj; j < std::min(nT, sj + g); ++j)
-        for (int64_t i = si; i < std::min(j + 1, si + g); ++i)
-          v.push_back((uint32_t)((i << 16) | j));
-  return v;
-}
 
 template <typename T>
 TrainWs<T> carve_train(const Geometry& g, void* base) {
@@ -412,27 +399,26 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   return a;
 }
 
-// Upload the tile visit order into the workspace (once per call).
+// The tile visit order, written into the workspace on the device (once per call).
 template <typename T>
-int upload_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
+int make_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
   if (LSSVM_TILE_GROUP <= 0 || g.nT == 0) return LSSVM_OK;
-  const std::vector<uint32_t> v = tile_order(g.nT, LSSVM_TILE_GROUP);
-  LSSVM_HIP(hipMemcpyAsync(w.order, v.data(), v.size() * sizeof(uint32_t),
-                           hipMemcpyHostToDevice, s));
-  LSSVM_HIP(hipStreamSynchronize(s));
+  LSSVM_HIP(launch_tile_order(g.nT, LSSVM_TILE_GROUP, w.order, s));
   return LSSVM_OK;
 }
 
-// a1 + a2: layout, norms, q and k_mm (left on the device); reads back the
-// input flags.
+// a1 + a2: layout, norms, q and k_mm (left on the device). With check set,
+// reads back the input flags and reports a non-finite X; otherwise the
+// caller reads them back with its next result.
 template <typename T>
 int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
-                 const lssvm_params& kp, hipStream_t s) {
-  LSSVM_TRY(upload_order<T>(g, w, s));
+                 const lssvm_params& kp, hipStream_t s, bool check = true) {
+  LSSVM_TRY(make_order<T>(g, w, s));
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
   LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
                               kp.degree, w.norms, w.q64, w.scal, s));
+  if (!check) return LSSVM_OK;
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipStreamSynchronize(s));
@@ -481,7 +467,7 @@ int timed_matvec(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
                  const double* p, hipStream_t s, MatvecTimer& tm, int64_t iter) {
   LSSVM_HIP(tm.start(s, iter));
   TileArgs<T> a = sym_args<T>(g, w, kp, kernel, p);
-  a.status = w.scal + S_STATUS;   // skip the launches once CG has stopped
+  a.stop = w.scal + S_STATUS + ST_DONE;   // skip the launches once CG has stopped
   LSSVM_HIP(launch_product<T>(g, a, kernel, w.gpart, s));
   LSSVM_HIP(tm.stop(s));
   return LSSVM_OK;
@@ -528,14 +514,15 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     return LSSVM_OK;
   }
 
-  // ---- setup: a1, a2, a3
-  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
+  // ---- setup: a1, a2, a3 (one read-back for the input flags and r0^T r0)
+  LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, /*check=*/false));
   LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.bp0, w.flags, s));
   LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
   LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
   LSSVM_HIP(hipStreamSynchronize(s));
+  if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
   if (g_host.flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
   const double delta0 = g_host.p[0];
   const double t_setup = ms_since(t0);

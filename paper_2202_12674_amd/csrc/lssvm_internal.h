@@ -7,19 +7,10 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "tile_args.h"
+
 namespace lssvm {
 
-enum Kern : int { KLIN = 0, KPOLY = 1, KRBF = 2 };
-
-// Points per tile edge and features per staged block, per element type
-// (compile-time, like the block sizes of Sec. III-C4). The symmetric schedule
-// needs square tiles.
-#ifndef LSSVM_F32_BK
-#define LSSVM_F32_BK 32
-#endif
-#ifndef LSSVM_F64_BK
-#define LSSVM_F64_BK 16
-#endif
 // Symmetric tiles are visited in GROUP x GROUP super-tiles of the upper
 // triangle, and each of the 8 XCDs takes a contiguous run of that order, so
 // the workgroups resident on one XCD share few point panels in its L2.
@@ -27,11 +18,6 @@ enum Kern : int { KLIN = 0, KPOLY = 1, KRBF = 2 };
 #ifndef LSSVM_TILE_GROUP
 #define LSSVM_TILE_GROUP 8
 #endif
-constexpr int kNumXcd = 8;
-
-template <typename T> struct TileShape;
-template <> struct TileShape<float> { static constexpr int T = 128, BK = LSSVM_F32_BK; };
-template <> struct TileShape<double> { static constexpr int T = 128, BK = LSSVM_F64_BK; };
 
 // Slots of the small fp64 scalar area in the workspace.
 enum Scalar : int {
@@ -73,43 +59,6 @@ inline int64_t cg_blocks(int64_t NP) {
 // Flags raised by kernels (int32 each).
 enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
 
-// What a symmetric tile launch computes: whole tiles, parked feature splits
-// of tiles (their raw inner products), or the fixup that sums a tile's parked
-// splits and finishes it.
-enum TilePart : int { kWhole = 0, kPartial = 1, kFixup = 2 };
-
-template <typename T>
-struct TileArgs {
-  const T* A;    // panel-major feature-blocked row points (see k_layout)
-  const T* B;    // panel-major feature-blocked column points
-  int64_t lda, ldb;
-  int64_t nkb;   // feature blocks of BK (even)
-  const T* nA;   // squared norms of row points (RBF)
-  const T* nB;   // squared norms of column points (RBF)
-  const double* pv;   // symmetric mode: the vector multiplied (fp64), zero beyond N
-  const double* q64;  // symmetric mode: q_i = k(x_i, x_m), zero beyond N
-  double* pq;         // symmetric mode: per panel I, sum p_j at [I], sum q_j p_j at [nTc + I]
-  const T* wB;        // general mode: per-column weights (alpha)
-  T gamma, coef0;
-  T rbf_scale;   // RBF exponent scale: gamma (fp64, exp) or gamma log2(e) (fp32, exp2)
-  int degree;
-  int64_t nTc;   // column tiles (general mode); tiles per side (symmetric mode)
-  int64_t ksplit;  // symmetric mode: workgroups per tile, each over nkb / ksplit feature
-                   // blocks (an even count). Linear kernel, whole tiles: row partials
-                   // of tile (I, J) and split s go to slot J ksplit + s, column
-                   // partials to I ksplit + s. Split launches park inner products in
-                   // gpart instead and a fixup launch finishes each tile.
-  int64_t tile_offset;  // symmetric mode: first tile of the launch in the visit order
-  T* gpart;             // split launches: parked inner products, ksplit 128^2 per tile
-  const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
-  double* part;  // partial sums, part[slot * part_ld + row]
-  const double* status;  // symmetric mode: CG status (skip the launch once done) or null
-  int64_t part_ld;
-  // A product's tiles may outnumber one launch (the dispatch grid counts work
-  // items in 32 bits), so the launcher splits them into chunks: workgroup b of
-  // a chunk takes tile slot tile_base + b of ntiles.
-  int64_t tile_base, ntiles;
-};
 
 // The rank-one and diagonal terms of Q~ p that the symmetric tiles leave out
 // (Eq. (13)): (Q~ p)_i = (K p)_i + (Q_mm - q_i) S - T + p_i / C for i < N,
@@ -124,6 +73,10 @@ struct RankOne {
   const double* scal;  // k(x_m, x_m) at S_KMM
   double invC;
 };
+
+// The symmetric tiles' visit order (GROUP x GROUP super-tiles), packed
+// (I << 16) | J, nT (nT + 1) / 2 entries.
+hipError_t launch_tile_order(int64_t nT, int64_t group, uint32_t* order, hipStream_t s);
 
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,

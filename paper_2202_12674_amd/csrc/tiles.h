@@ -1,11 +1,12 @@
 // The a4 / a7 tile kernel: the kernel-matrix part K p of the implicit Q~
 // product (Eqs. (13), (16)) and the decision values on the gfx950 matrix
 // cores, one 128 x 128 tile of points per workgroup. Included by kernels.hip
-// (one translation unit); kept on its own
-// so that the tile kernel's source can be identified apart from the rest.
+// (one translation unit); kept on its own, with its interface in
+// tile_args.h, so that the tile kernel's code can be identified apart from
+// the rest.
 #pragma once
 
-#include "lssvm_internal.h"
+#include "tile_args.h"
 
 #include <hip/hip_runtime.h>
 
@@ -231,7 +232,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ double red_c[WAVES_M][BM];
 
   if constexpr (SYM) {
-    if (a.status && a.status[ST_DONE] != 0.0) return;   // CG already stopped
+    if (a.stop && *a.stop != 0.0) return;   // CG already stopped
   }
   int64_t I, J;
   // Symmetric tiles may have their features split over KS workgroups. For
