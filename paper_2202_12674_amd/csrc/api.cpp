@@ -10,13 +10,13 @@
 
 #include <algorithm>
 #include <chrono>
-#include <vector>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
 
 namespace lssvm {
 
