@@ -239,6 +239,42 @@ def fp32_sensitivity(X, cfg):
     return float(v @ (Qt @ v)) * cfg.C * 2.0 ** -24
 
 
+def _random_large_cases(count=16, seed=11):
+    """Seeded large shapes (2000..40000 points, 100..5000 features, log-uniform),
+    random kernel parameters and C from 0.01 to 100."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        n = int(np.exp(rng.uniform(np.log(2000), np.log(40000))))
+        d = int(np.exp(rng.uniform(np.log(100), np.log(5000))))
+        kernel = ["linear", "poly", "rbf"][rng.integers(3)]
+        dtype = ["f64", "f32"][rng.integers(2)]
+        C = float(10 ** rng.uniform(-2, 2))
+        kp = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=float(rng.choice([0.0, 1.0])),
+                                       degree=int(rng.integers(1, 5))),
+                  rbf=dict(gamma=float(10 ** rng.uniform(-1, 0.5)) / d))[kernel]
+        out.append((kernel, dtype, n, d, C, kp))
+    return out
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d,C,kp", _random_large_cases())
+def test_matvec_random_large(torch_dev, kernel, dtype, n, d, C, kp):
+    """Large random shapes: 64 sampled rows (the first and the last among them)
+    against the oracle's rows of Q~."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = S.Config(f"{kernel}_{dtype}_{n}x{d}", dtype, kernel, n, d, mu=1.0, inf_frac=0.5,
+                   flip_frac=0.05, C=C, eps=1e-8, **kp)
+    log(f"matvec random large {cfg.name} C={C:.3g} {kp}")
+    X, _, _ = S.make_train(cfg)
+    p = S.probe_vector(n - 1, cfg.np_dtype, seed=n)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=C, **kw_of(cfg)).cpu().numpy()
+    rows = np.unique(np.concatenate([[0, n - 2],
+                                     np.random.default_rng(n).choice(n - 1, 62, replace=False)]))
+    ref = O.reduced_rows(X.astype(np.float64), spec_of(cfg), C, rows) @ p.astype(np.float64)
+    assert rel_err(out[rows], ref) <= TOL_MV[dtype]
+
+
 @pytest.mark.parametrize("kernel,dtype,n,d,C", [_random_cases()[k] for k in (0, 4, 8, 13, 17, 21)])
 def test_train_random_shapes(torch_dev, kernel, dtype, n, d, C):
     """The full alpha / b bar where fp32 can resolve the solution to it
