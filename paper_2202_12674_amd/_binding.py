@@ -159,6 +159,39 @@ def _dev_ptr(t, name: str):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _matrix(t, name: str):
+    """(rows, columns) of a 2-D tensor, else TypeError / ValueError."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D (points x features), not {tuple(t.shape)}")
+    return t.shape
+
+
+def _expect(t, name: str, shape: tuple, like, like_name: str = "X") -> None:
+    """Refuse t unless it has the given shape and the dtype and device of
+    `like`: a vector shorter than the sizes passed to the library would be read
+    or written past its end on the device, so this runs before any call."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if tuple(t.shape) != tuple(shape) or t.dtype != like.dtype or t.device != like.device:
+        raise ValueError(f"{name} must have shape {tuple(shape)} and the dtype and device of "
+                         f"{like_name}, not {tuple(t.shape)} {t.dtype} on {t.device}")
+
+
+def _workspace(ws, device):
+    torch = _torch()
+    if not isinstance(ws, torch.Tensor) or ws.device != device:
+        raise ValueError(f"workspace must be a tensor on {device}")
+    return ws
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
 def _stream(device):
     torch = _torch()
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
@@ -215,19 +248,20 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
     alpha0 (device tensor, n values): start CG from its first n - 1 entries
     (a previous solution or a saved iterate) instead of zero."""
     torch = _torch()
-    n, d = X.shape
+    n, d = _matrix(X, "X")
     dt = _dtype_code(X)
-    if y.dtype != X.dtype or y.shape != (n,):
-        raise ValueError("y must have shape (n,) and the dtype of X")
+    _expect(y, "y", (n,), X)
+    if alpha0 is not None:
+        _expect(alpha0, "alpha0", (n,), X)
     k, kp = _params(kernel, gamma, coef0, degree)
     if workspace is None:
         workspace = alloc_workspace(lib().lssvm_workspace_bytes(n, d, dt), X.device)
+    _workspace(workspace, X.device)
+    _dev_ptr(X, "X")
     alpha = torch.empty(n, dtype=X.dtype, device=X.device)
     b = ctypes.c_double(0.0)
     info = Info()
     if alpha0 is not None:
-        if alpha0.shape != (n,) or alpha0.dtype != X.dtype or alpha0.device != X.device:
-            raise ValueError("alpha0 must have shape (n,) and the dtype and device of X")
         alpha.copy_(alpha0)
         info.warm_start = 1
     info.compute_true_residual = 1 if true_residual else 0
@@ -238,7 +272,7 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
         info.history_capacity = history
     code = lib().lssvm_train(_dev_ptr(X, "X"), _dev_ptr(y, "y"), n, d, dt, k, ctypes.byref(kp),
                              float(C), float(eps), int(max_iter), _dev_ptr(workspace, "workspace"),
-                             workspace.numel(), _dev_ptr(alpha, "alpha"), ctypes.byref(b),
+                             _nbytes(workspace), _dev_ptr(alpha, "alpha"), ctypes.byref(b),
                              ctypes.byref(info), _stream(X.device))
     _check(code, allow_not_converged=not raise_not_converged)
     return TrainResult(alpha, b.value, code, code == OK, info.iterations, info.n_matvec,
@@ -252,18 +286,22 @@ def predict(X_train, alpha, b: float, X_test, kernel: str = "linear", gamma: flo
             coef0: float = 0.0, degree: int = 1, workspace=None, want_labels: bool = True):
     """lssvm_predict: (scores, labels) for the rows of X_test."""
     torch = _torch()
-    n, d = X_train.shape
-    nt = X_test.shape[0]
+    n, d = _matrix(X_train, "X_train")
+    nt, dx = _matrix(X_test, "X_test")
     dt = _dtype_code(X_train)
+    _expect(alpha, "alpha", (n,), X_train, "X_train")
+    _expect(X_test, "X_test", (nt, d), X_train, "X_train")
     k, kp = _params(kernel, gamma, coef0, degree)
     if workspace is None:
         workspace = alloc_workspace(lib().lssvm_predict_workspace_bytes(n, nt, d, dt),
                                     X_train.device)
+    _workspace(workspace, X_train.device)
+    _dev_ptr(X_train, "X_train")
     scores = torch.empty(nt, dtype=X_train.dtype, device=X_train.device)
     labels = torch.empty(nt, dtype=torch.int32, device=X_train.device) if want_labels else None
     code = lib().lssvm_predict(_dev_ptr(X_train, "X_train"), _dev_ptr(alpha, "alpha"), float(b),
                                n, d, dt, k, ctypes.byref(kp), _dev_ptr(X_test, "X_test"), nt,
-                               _dev_ptr(workspace, "workspace"), workspace.numel(),
+                               _dev_ptr(workspace, "workspace"), _nbytes(workspace),
                                _dev_ptr(scores, "scores"),
                                _dev_ptr(labels, "labels") if labels is not None else None,
                                _stream(X_train.device))
@@ -275,16 +313,21 @@ def matvec(X, p, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
            degree: int = 1, C: float = 1.0, workspace=None, out=None):
     """lssvm_matvec: out = Q~ p for the reduced system of the points X."""
     torch = _torch()
-    n, d = X.shape
+    n, d = _matrix(X, "X")
     dt = _dtype_code(X)
+    _expect(p, "p", (n - 1,), X)
+    if out is not None:
+        _expect(out, "out", (n - 1,), X)
     k, kp = _params(kernel, gamma, coef0, degree)
     if workspace is None:
         workspace = alloc_workspace(lib().lssvm_workspace_bytes(n, d, dt), X.device)
+    _workspace(workspace, X.device)
+    _dev_ptr(X, "X")
     if out is None:
         out = torch.empty(n - 1, dtype=X.dtype, device=X.device)
     code = lib().lssvm_matvec(_dev_ptr(X, "X"), n, d, dt, k, ctypes.byref(kp), float(C),
                               _dev_ptr(p, "p"), _dev_ptr(out, "out"),
-                              _dev_ptr(workspace, "workspace"), workspace.numel(),
+                              _dev_ptr(workspace, "workspace"), _nbytes(workspace),
                               _stream(X.device))
     _check(code)
     return out
@@ -301,11 +344,14 @@ def cg_step(x, r, d, q, scalars, workspace=None):
             raise TypeError(f"{nm} must be float64")
     if not (r.numel() == d.numel() == q.numel() == N) or scalars.numel() < 4:
         raise ValueError("x, r, d, q need equal lengths and scalars 4 entries")
+    if any(t.device != x.device for t in (r, d, q, scalars)):
+        raise ValueError("x, r, d, q and scalars must be on one device")
     if workspace is None:
         workspace = alloc_workspace(lib().lssvm_cg_step_workspace_bytes(N), x.device)
+    _workspace(workspace, x.device)
     _check(lib().lssvm_cg_step(N, _dev_ptr(x, "x"), _dev_ptr(r, "r"), _dev_ptr(d, "d"),
                                _dev_ptr(q, "q"), _dev_ptr(scalars, "scalars"),
-                               _dev_ptr(workspace, "workspace"), workspace.numel(),
+                               _dev_ptr(workspace, "workspace"), _nbytes(workspace),
                                _stream(x.device)))
 
 
@@ -316,6 +362,6 @@ def mfma_peak(dtype, device) -> float:
     code = F64 if dtype == torch.float64 else F32
     ws = alloc_workspace(lib().lssvm_mfma_peak_workspace_bytes(), device)
     out = ctypes.c_double(0.0)
-    _check(lib().lssvm_mfma_peak(code, _dev_ptr(ws, "workspace"), ws.numel(), ctypes.byref(out),
+    _check(lib().lssvm_mfma_peak(code, _dev_ptr(ws, "workspace"), _nbytes(ws), ctypes.byref(out),
                                  _stream(device)))
     return out.value

@@ -154,6 +154,43 @@ def test_binding_refuses_cpu_tensors():
         P.train(X, y, workspace=torch.zeros(1 << 16, dtype=torch.uint8))
 
 
+def test_binding_checks_shapes_before_the_device():
+    # Sizes the library is given come from X; a shorter p, out, alpha or
+    # X_test would be read or written past its end on the device, so the
+    # binding refuses them before any call (CPU tensors reach these checks).
+    import torch
+    f64, f32 = torch.float64, torch.float32
+    X = torch.zeros(6, 3, dtype=f64)
+    ws = torch.zeros(256, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="p must have shape"):
+        P.matvec(X, torch.zeros(4, dtype=f64), workspace=ws)
+    with pytest.raises(ValueError, match="p must have shape"):
+        P.matvec(X, torch.zeros(5, dtype=f32), workspace=ws)
+    with pytest.raises(ValueError, match="out must have shape"):
+        P.matvec(X, torch.zeros(5, dtype=f64), workspace=ws, out=torch.zeros(4, dtype=f64))
+    with pytest.raises(ValueError, match="2-D"):
+        P.matvec(torch.zeros(6, dtype=f64), torch.zeros(5, dtype=f64), workspace=ws)
+    with pytest.raises(ValueError, match="y must have shape"):
+        P.train(X, torch.ones(5, dtype=f64), workspace=ws)
+    with pytest.raises(ValueError, match="y must have shape"):
+        P.train(X, torch.ones(6, dtype=f32), workspace=ws)
+    with pytest.raises(ValueError, match="alpha0 must have shape"):
+        P.train(X, torch.ones(6, dtype=f64), workspace=ws, alpha0=torch.zeros(5, dtype=f64))
+    with pytest.raises(ValueError, match="alpha must have shape"):
+        P.predict(X, torch.zeros(5, dtype=f64), 0.0, torch.zeros(2, 3, dtype=f64), workspace=ws)
+    with pytest.raises(ValueError, match="X_test must have shape"):
+        P.predict(X, torch.zeros(6, dtype=f64), 0.0, torch.zeros(2, 4, dtype=f64), workspace=ws)
+    with pytest.raises(ValueError, match="X_test must have shape"):
+        P.predict(X, torch.zeros(6, dtype=f64), 0.0, torch.zeros(2, 3, dtype=f32), workspace=ws)
+    with pytest.raises(TypeError):
+        P.matvec(X.to(torch.int32), torch.zeros(5, dtype=torch.int32), workspace=ws)
+    # well-shaped CPU tensors pass the shape checks and stop at the device check
+    with pytest.raises(TypeError, match="GPU tensor"):
+        P.matvec(X, torch.zeros(5, dtype=f64), workspace=ws)
+    with pytest.raises(TypeError, match="GPU tensor"):
+        P.predict(X, torch.zeros(6, dtype=f64), 0.0, torch.zeros(2, 3, dtype=f64), workspace=ws)
+
+
 def test_last_error_is_thread_local():
     import threading
     _train(n=0)
