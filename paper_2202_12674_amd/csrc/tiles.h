@@ -230,6 +230,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ __attribute__((aligned(16))) T Bs1[CHUNKS * VEC];
   __shared__ double red_r[WAVES_N][BM];
   __shared__ double red_c[WAVES_M][BM];
+  // fp32: the tile's panel vectors are staged with its first feature block,
+  // so the epilogue reads no global memory (its loads of p and the norms
+  // otherwise cost several L2 round trips per tile: up to 10% of the product
+  // at 64 features, 0.5% at 4096). p over rows I and over columns J
+  // (symmetric mode) go to vp; the squared norms of both panels (radial
+  // kernel) and the column weights (general mode) to vt[0], vt[1], vt[2].
+  // fp64 reads them from global memory: staged, it measured 0.5-4% slower.
+  constexpr bool kVecLds = sizeof(T) == 4;
+  __shared__ __attribute__((aligned(16))) double vp[SYM ? 2 : 1][BM];
+  __shared__ __attribute__((aligned(16))) T vt[3][BM];
 
   if constexpr (SYM) {
     if (a.stop && *a.stop != 0.0) return;   // CG already stopped
@@ -311,6 +321,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
   };
 
+  // One 16-byte piece per lane: a wave moves a 1 KiB vector (128 doubles) or
+  // a T vector of 128 entries with lanes beyond it idle. Every vector is
+  // padded to whole panels, so the pieces stay inside it.
+  auto dvec = [&]() {
+    if constexpr (!kVecLds) return;
+    constexpr int TL = BM * (int)sizeof(T) / 16;   // lanes per T vector
+    constexpr int TE = 16 / (int)sizeof(T);        // T entries per lane
+    if constexpr (SYM) {
+      if (wave == 0)
+        __builtin_amdgcn_global_load_lds((gptr_t)(a.pv + I * BM + 2 * lane), (lptr_t)&vp[0][0],
+                                         16, 0, 0);
+      else if (wave == 1)
+        __builtin_amdgcn_global_load_lds((gptr_t)(a.pv + J * BM + 2 * lane), (lptr_t)&vp[1][0],
+                                         16, 0, 0);
+    } else {
+      if (wave == 0 && lane < TL)
+        __builtin_amdgcn_global_load_lds((gptr_t)(a.wB + J * BM + TE * lane), (lptr_t)&vt[2][0],
+                                         16, 0, 0);
+    }
+    if constexpr (KER == KRBF) {
+      if (wave == 2 && lane < TL)
+        __builtin_amdgcn_global_load_lds((gptr_t)(a.nA + I * BM + TE * lane), (lptr_t)&vt[0][0],
+                                         16, 0, 0);
+      else if (wave == 3 && lane < TL)
+        __builtin_amdgcn_global_load_lds((gptr_t)(a.nB + J * BM + TE * lane), (lptr_t)&vt[1][0],
+                                         16, 0, 0);
+    }
+  };
+
   typename MF::acc_t acc[RB][CB];
 #pragma unroll
   for (int i = 0; i < RB; ++i)
@@ -362,6 +401,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   constexpr bool kPinLoads = sizeof(T) == 4, kPinWait = sizeof(T) == 8;
   if constexpr (PART != kFixup) {
   dload(0, As0, Bs0);
+  if constexpr (PART == kWhole) dvec();
   vm_wait_all();
   __syncthreads();
   for (int64_t kb = 0; kb < nkb; kb += 2) {
@@ -406,6 +446,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
           }
       return;
     } else {
+      if constexpr (kVecLds) {
+        dvec();
+        vm_wait_all();
+        __syncthreads();
+      }
       for (int64_t s2 = 0; s2 < KS; ++s2) {
 #pragma unroll
         for (int i = 0; i < RB; ++i)
@@ -432,10 +477,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   double pBj[CB];
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
-    const int64_t gj = J * BM + wn * C::WN + j * MF::M + cl;
-    nBj[j] = (KER == KRBF) ? a.nB[gj] : T(0);
-    if constexpr (SYM) pBj[j] = a.pv[gj];
-    else pBj[j] = (double)a.wB[gj];
+    const int lj = wn * C::WN + j * MF::M + cl;
+    const int64_t gj = J * BM + lj;
+    nBj[j] = (KER == KRBF) ? (kVecLds ? vt[1][lj] : a.nB[gj]) : T(0);
+    if constexpr (SYM) pBj[j] = kVecLds ? vp[1][lj] : a.pv[gj];
+    else pBj[j] = kVecLds ? (double)vt[2][lj] : (double)a.wB[gj];
   }
   double cs[CB];
 #pragma unroll
@@ -456,9 +502,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     double pAi[VH];
 #pragma unroll
     for (int vv = 0; vv < VH; ++vv) {
-      const int64_t gi = I * BM + wm * C::WM + i * MF::M + MF::row(v0 + vv, lane);
-      const T nAi = (KER == KRBF) ? a.nA[gi] : T(0);
-      pAi[vv] = SYM ? a.pv[gi] : 0.0;
+      const int li = wm * C::WM + i * MF::M + MF::row(v0 + vv, lane);
+      const int64_t gi = I * BM + li;
+      const T nAi = (KER == KRBF) ? (kVecLds ? vt[0][li] : a.nA[gi]) : T(0);
+      pAi[vv] = SYM ? (kVecLds ? vp[0][li] : a.pv[gi]) : 0.0;
 #pragma unroll
       for (int j = 0; j < CB; ++j)
         kv[vv][j] = kernel_value<KER, T>(acc[i][j][v0 + vv], nAi, nBj[j], a.gamma, a.coef0,
@@ -545,7 +592,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       double sp = 0.0, sq = 0.0;
       if (tid < BM) {
         const int64_t j = I * BM + tid;
-        sp = a.pv[j];
+        sp = kVecLds ? vp[0][tid] : a.pv[j];
         sq = a.q64[j] * sp;
       }
 #pragma unroll
