@@ -275,6 +275,47 @@ def test_matvec_random_large(torch_dev, kernel, dtype, n, d, C, kp):
     assert rel_err(out[rows], ref) <= TOL_MV[dtype]
 
 
+# Extreme aspect ratios: few points with many features (long feature loops;
+# the linear kernel at its largest feature splits), and tens of thousands of
+# points with one to three features (one feature block per tile, every
+# workgroup's time in its first block and epilogue).
+EXTREME_SHAPES = [("linear", "f64", 300, 65536), ("rbf", "f32", 700, 30000),
+                  ("poly", "f64", 1000, 16384), ("linear", "f32", 40000, 1),
+                  ("rbf", "f64", 33000, 2), ("poly", "f32", 20000, 3)]
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d", EXTREME_SHAPES)
+def test_matvec_extreme_shapes(torch_dev, kernel, dtype, n, d):
+    """64 sampled rows (the first and the last among them) against the
+    oracle's rows of Q~."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=1.0)
+    log(f"matvec extreme {cfg.name}")
+    X, _, _ = S.make_train(cfg)
+    p = S.probe_vector(n - 1, cfg.np_dtype, seed=n)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=cfg.C,
+                   **kw_of(cfg)).cpu().numpy()
+    rows = np.unique(np.concatenate([[0, n - 2],
+                                     np.random.default_rng(n).choice(n - 1, 62, replace=False)]))
+    ref = O.reduced_rows(X.astype(np.float64), spec_of(cfg), cfg.C, rows) @ p.astype(np.float64)
+    assert rel_err(out[rows], ref) <= TOL_MV[dtype]
+
+
+@pytest.mark.parametrize("kernel,dtype", [("linear", "f64"), ("rbf", "f32")])
+def test_train_wide(torch_dev, kernel, dtype):
+    """300 points with 16384 features: the solution, bias and test labels
+    against the oracle's CG."""
+    torch, dev = torch_dev
+    cfg = small_cfg(kernel, dtype, 300, 16384)
+    log(f"train wide {cfg.name}")
+    X, y, scale = S.make_train(cfg)
+    Xte, _ = S.make_test(cfg, scale, n_test=200)
+    alpha, b, iters, spread = oracle_cg_with_spread(cfg, X, y)
+    f_te = O.decision(X, alpha, b, Xte, spec_of(cfg))
+    check_train(torch, dev, cfg, alpha, b, iters, X, y, Xte, f_te, spread)
+
+
 @pytest.mark.parametrize("kernel,dtype,n,d,C", [_random_cases()[k] for k in (0, 4, 8, 13, 17, 21)])
 def test_train_random_shapes(torch_dev, kernel, dtype, n, d, C):
     """The full alpha / b bar where fp32 can resolve the solution to it
