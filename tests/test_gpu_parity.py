@@ -558,6 +558,44 @@ def test_predict_oracle_model(torch_dev, dtype, kernel, n, nt, d):
 
 # ----------------------------------------------------- edge / errors --------
 
+def test_train_concurrent_threads(torch_dev):
+    """Two host threads train different problems at once, each on a stream of
+    its own: the library keeps its host-side state per thread and the caller
+    owns every device buffer, so each result equals its sequential run bit for
+    bit."""
+    import threading
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfgs = [small_cfg("rbf", "f64", 1500, 40), small_cfg("poly", "f32", 2000, 100)]
+    inputs = []
+    for c in cfgs:
+        X, y, _ = S.make_train(c)
+        inputs.append((c, to_dev(torch, dev, X), to_dev(torch, dev, y)))
+    seq = [P.train(X, y, C=c.C, eps=c.eps, **kw_of(c)) for c, X, y in inputs]
+    torch.cuda.synchronize()
+    out, errors = [None] * len(inputs), []
+
+    def run(k):
+        try:
+            c, X, y = inputs[k]
+            st = torch.cuda.Stream(device=dev)
+            with torch.cuda.stream(st):
+                out[k] = P.train(X, y, C=c.C, eps=c.eps, **kw_of(c))
+            st.synchronize()
+        except Exception as e:   # reported below, in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=run, args=(k,)) for k in range(len(inputs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for a, b in zip(seq, out):
+        assert b.converged and a.iterations == b.iterations
+        assert torch.equal(a.alpha, b.alpha) and a.b == b.b
+
+
 def test_train_single_point_and_equal_labels(torch_dev):
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
