@@ -246,7 +246,7 @@ def main():
 
     def step():
         r = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, max_iter=cfg.max_iter, workspace=ws,
-                    time_matvec=True, **kw)
+                    time_matvec=True, matvec_times=4096, **kw)
         t0 = time.perf_counter()
         P.predict(Xd, r.alpha, r.b, Xted, workspace=wsp, **kw)   # returns after the GPU work
         pred_ms.append((time.perf_counter() - t0) * 1e3)
@@ -278,6 +278,7 @@ def main():
     ms_per_step = total_ms / args.steps
     value = step_flops / (total_ms * 1e-3) / 1e9
     mv_ms = sum(r.t_matvec_ms for r in results) / max(1, sum(r.n_matvec_timed for r in results))
+    mv_each = [t for r in results for t in r.matvec_times]   # every timed product, in order
     achieved = mv_flops / (mv_ms * 1e-3) / 1e12
     peak = PEAK_TFLOPS[cfg.dtype]
     measured_peak = P.mfma_peak(Xd.dtype, dev)
@@ -306,6 +307,10 @@ def main():
         "cg_iterations": results[-1].iterations,
         "n_matvec_per_step": results[-1].n_matvec,
         "matvec_ms": round(mv_ms, 4),
+        "matvec_median_ms": round(statistics.median(mv_each), 4) if mv_each else None,
+        "matvec_cov": (round(statistics.pstdev(mv_each) / statistics.mean(mv_each), 4)
+                       if len(mv_each) > 1 else None),
+        "matvec_reps": len(mv_each),
         "matvec_gflops": round(mv_flops / (mv_ms * 1e-3) / 1e9, 2),
         "matvec_dense_equiv_gflops": round(2 * N * N * cfg.d / (mv_ms * 1e-3) / 1e9, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,

@@ -93,6 +93,10 @@ typedef struct lssvm_info {
     int32_t reserved2;
     double t_matvec_ms;            /* sum of the timed Q~ products (tile kernel only) */
     int64_t n_matvec_timed;        /* number of products in t_matvec_ms              */
+    double* matvec_times;          /* in: host array or NULL; receives the duration in
+                                      ms of each timed product, in order, up to
+                                      matvec_times_capacity of them (time_matvec) */
+    int64_t matvec_times_capacity; /* in: length of matvec_times                     */
 } lssvm_info;
 
 /* Device workspace needed by lssvm_train and lssvm_matvec for n points of

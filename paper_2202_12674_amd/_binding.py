@@ -36,7 +36,9 @@ class Info(ctypes.Structure):
                 ("residual_history", ctypes.POINTER(ctypes.c_double)),
                 ("history_capacity", ctypes.c_int64), ("time_matvec", ctypes.c_int32),
                 ("reserved2", ctypes.c_int32), ("t_matvec_ms", ctypes.c_double),
-                ("n_matvec_timed", ctypes.c_int64)]
+                ("n_matvec_timed", ctypes.c_int64),
+                ("matvec_times", ctypes.POINTER(ctypes.c_double)),
+                ("matvec_times_capacity", ctypes.c_int64)]
 
 
 class LssvmError(RuntimeError):
@@ -236,17 +238,20 @@ class TrainResult:
     history: list
     t_matvec_ms: float = 0.0
     n_matvec_timed: int = 0
+    matvec_times: list = dataclasses.field(default_factory=list)   # ms per timed product
 
 
 def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
           degree: int = 1, C: float = 1.0, eps: float = 1e-8, max_iter: int = 0,
           workspace=None, true_residual: bool = False, history: int = 0,
           raise_not_converged: bool = False, time_matvec: bool = False,
-          alpha0=None) -> TrainResult:
+          alpha0=None, matvec_times: int = 0) -> TrainResult:
     """lssvm_train on device tensors X (n x d) and y (n,), same float dtype.
 
     alpha0 (device tensor, n values): start CG from its first n - 1 entries
-    (a previous solution or a saved iterate) instead of zero."""
+    (a previous solution or a saved iterate) instead of zero. With
+    time_matvec, matvec_times > 0 returns the duration of each of the first
+    that many products as well as their sum."""
     torch = _torch()
     n, d = _matrix(X, "X")
     dt = _dtype_code(X)
@@ -270,6 +275,10 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
     if hist is not None:
         info.residual_history = ctypes.cast(hist, ctypes.POINTER(ctypes.c_double))
         info.history_capacity = history
+    times = (ctypes.c_double * matvec_times)() if matvec_times > 0 else None
+    if times is not None:
+        info.matvec_times = ctypes.cast(times, ctypes.POINTER(ctypes.c_double))
+        info.matvec_times_capacity = matvec_times
     code = lib().lssvm_train(_dev_ptr(X, "X"), _dev_ptr(y, "y"), n, d, dt, k, ctypes.byref(kp),
                              float(C), float(eps), int(max_iter), _dev_ptr(workspace, "workspace"),
                              _nbytes(workspace), _dev_ptr(alpha, "alpha"), ctypes.byref(b),
@@ -279,7 +288,9 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
                        info.rel_residual, info.true_rel_residual, info.t_setup_ms, info.t_cg_ms,
                        info.t_total_ms,
                        list(hist[:min(history, info.iterations)]) if hist is not None else [],
-                       info.t_matvec_ms, info.n_matvec_timed)
+                       info.t_matvec_ms, info.n_matvec_timed,
+                       list(times[:min(matvec_times, info.n_matvec_timed)])
+                       if times is not None else [])
 
 
 def predict(X_train, alpha, b: float, X_test, kernel: str = "linear", gamma: float = 1.0,

@@ -278,8 +278,12 @@ struct MatvecTimer {
   int used = 0;          // event pairs recorded since the last harvest
   double total_ms = 0.0;
   int64_t count = 0;
-  hipError_t init(bool enable) {
+  double* out = nullptr;   // caller's array of per-product times, or null
+  int64_t cap = 0;
+  hipError_t init(bool enable, double* times = nullptr, int64_t capacity = 0) {
     on = enable;
+    out = times;
+    cap = capacity;
     if (!on) return hipSuccess;
     int device = 0;
     hipError_t r = hipGetDevice(&device);
@@ -319,6 +323,7 @@ struct MatvecTimer {
       hipError_t r = hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]);
       if (r != hipSuccess) return r;
       total_ms += ms;
+      if (out && count < cap) out[count] = ms;
       ++count;
     }
     used = 0;
@@ -527,7 +532,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   const double delta0 = g_host.p[0];
   const double t_setup = ms_since(t0);
   MatvecTimer tm;
-  LSSVM_HIP(tm.init(info && info->time_matvec));
+  LSSVM_HIP(tm.init(info && info->time_matvec, info ? info->matvec_times : nullptr,
+                    info ? info->matvec_times_capacity : 0));
 
   // ---- a4 + a5: conjugate gradients
   // Iterations are enqueued in batches (1, 2, 4, ... up to 32) and the status
@@ -861,6 +867,8 @@ int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtyp
     if (max_iter < 0) return fail(LSSVM_EINVAL, "max_iter must be >= 0");
     if (info && info->residual_history == nullptr && info->history_capacity != 0)
       return fail(LSSVM_EINVAL, "history_capacity without residual_history");
+    if (info && info->matvec_times == nullptr && info->matvec_times_capacity != 0)
+      return fail(LSSVM_EINVAL, "matvec_times_capacity without matvec_times");
     const lssvm_params p = params_or_default(kp);
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (dtype == LSSVM_F64)

@@ -109,6 +109,19 @@ def test_train_history_without_buffer():
     info.history_capacity = 5
     assert _train(info=ctypes.byref(info)) == B.EINVAL
     assert "history" in P.last_error()
+    info = B.Info()
+    info.matvec_times_capacity = 5
+    assert _train(info=ctypes.byref(info)) == B.EINVAL
+    assert "matvec_times" in P.last_error()
+
+
+def test_info_layout_matches_header():
+    """The binding's lssvm_info mirrors the header field for field."""
+    txt = open(HEADER).read()
+    body = re.search(r"typedef struct lssvm_info \{(.*?)\} lssvm_info;", txt, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = re.findall(r"(\w+)\s*;", body)
+    assert names == [f[0] for f in B.Info._fields_]
 
 
 def test_predict_rejects_bad_arguments():

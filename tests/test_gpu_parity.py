@@ -513,6 +513,24 @@ def test_train_residual_replacement(torch_dev):
     assert res.n_matvec == res.iterations + res.iterations // 50
 
 
+def test_train_matvec_times(torch_dev):
+    """Per-product times: one entry per timed product (the residual refresh
+    after 50 iterations included), each positive, summing to the reported
+    total; a short array takes the first products only."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("rbf", "f64", 700, 12, C=100.0, eps=1e-9)
+    X, y, _, _ = data_of(cfg)
+    Xd, yd = to_dev(torch, dev, X), to_dev(torch, dev, y)
+    r = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, time_matvec=True, matvec_times=1000, **kw_of(cfg))
+    assert r.iterations > 50 and r.iterations < r.n_matvec_timed <= r.n_matvec
+    assert len(r.matvec_times) == r.n_matvec_timed and min(r.matvec_times) > 0.0
+    assert sum(r.matvec_times) == pytest.approx(r.t_matvec_ms, rel=1e-12)
+    r5 = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, time_matvec=True, matvec_times=5, **kw_of(cfg))
+    assert len(r5.matvec_times) == 5 and r5.n_matvec_timed == r.n_matvec_timed
+    assert torch.equal(r5.alpha, r.alpha)
+
+
 @pytest.mark.parametrize("name", list(S.CONFIGS))
 def test_train_configs(torch_dev, name):
     torch, dev = torch_dev
