@@ -10,7 +10,10 @@ Prints one JSON line. `value` is the whole-step throughput in GFLOP/s with
 the symmetric count N(N+1)d per implicit product (N = n - 1) plus
 2 n_test n d for the prediction. `roofline` is the tile kernel's own rate:
 N(N+1)d divided by its average duration, measured with HIP events recorded
-on the launch stream over the timed steps. `a5_cg_vector_step` times the CG
+on the launch stream over the timed steps (`matvec_median_ms`, `matvec_cov`
+over every timed product). `time_to_eps_ms` is the median over the timed
+trainings (5 by default); one more untimed training reports the true
+relative residual. `a5_cg_vector_step` times the CG
 vector step alone (lssvm_cg_step, 11 passes of N doubles) on N = 2^26 against
 the HBM peak. `cpu_baseline` times the CPU oracle's explicit row-panel product
 on a bounded sample of the same workload.
@@ -180,7 +183,7 @@ def device_facts(torch, dev):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="poly_f32_32768x4096")
     ap.add_argument("--n-test", type=int, default=1024)
@@ -269,6 +272,10 @@ def main():
             f"wall {walls[-1]:.1f} ms")
     torch.cuda.synchronize()
     total_ms = (time.perf_counter() - t_all) * 1e3
+    # one more training, untimed, with the true residual ||rhs - Q~ x|| / ||rhs||
+    # (one extra product after the solve)
+    r_true = P.train(Xd, yd, C=cfg.C, eps=cfg.eps, max_iter=cfg.max_iter, workspace=ws,
+                     true_residual=True, **kw)
 
     N = cfg.n - 1
     mv_flops = N * (N + 1) * cfg.d
@@ -305,6 +312,10 @@ def main():
         "time_to_eps_cov": round(statistics.pstdev(train_ms) / statistics.mean(train_ms), 4),
         "predict_ms": round(statistics.median(pred_ms[args.warmup:] or pred_ms), 3),
         "cg_iterations": results[-1].iterations,
+        "cg_ms_per_iteration": round(statistics.median(train_ms) / max(1, results[-1].iterations),
+                                     3),
+        "rel_residual": r_true.rel_residual,
+        "true_rel_residual": r_true.true_rel_residual,
         "n_matvec_per_step": results[-1].n_matvec,
         "matvec_ms": round(mv_ms, 4),
         "matvec_median_ms": round(statistics.median(mv_each), 4) if mv_each else None,
