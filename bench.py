@@ -74,6 +74,28 @@ def traffic_record(workload: str):
     return rec.get("hbm_bytes_per_product")
 
 
+def host_facts():
+    """The host CPU's model name, its logical CPUs available to this process
+    and numpy's BLAS (name and version), as the oracle's timings depend on them."""
+    import numpy as np
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{b.get('name')} {b.get('version')}"
+    except Exception:  # noqa: BLE001
+        pass
+    return {"cpu_model": model, "cpus_available": len(os.sched_getaffinity(0)), "blas": blas}
+
+
 def cpu_baseline(cfg, X, budget_s: float):
     """The oracle's explicit row-panel product Q~[rows] @ p on the host cores."""
     import numpy as np
@@ -102,7 +124,7 @@ def cpu_baseline(cfg, X, budget_s: float):
     dt = time.perf_counter() - t0
     flops = rows_done * (N + 1) * cfg.d          # share of the symmetric count N(N+1)d
     return {"value": flops / dt / 1e9, "unit": "GFLOP/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_facts(),
             "sample": f"{rows_done} of {N} rows of the explicit reduced matrix (fp64, "
                       f"panels of {panel}) times a vector, {dt:.1f} s"}
 
