@@ -489,8 +489,8 @@ __global__ __launch_bounds__(256) void k_linear_w_sum(const double* __restrict__
 
 // One block per test point: f = <w, x> + b (fp64), label +1 iff f > 0.
 template <typename T>
-__global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte, int64_t n_test,
-                                                       int64_t d, const double* __restrict__ w,
+__global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte, int64_t d,
+                                                       const double* __restrict__ w,
                                                        double b, T* __restrict__ scores,
                                                        int32_t* __restrict__ labels,
                                                        int* __restrict__ flags) {
@@ -813,8 +813,8 @@ hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_
   hipLaunchKernelGGL(k_linear_w_sum, dim3(gx), dim3(NT), 0, s, part, nchunks, d, w);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_linear_scores<T>, dim3((unsigned)n_test), dim3(NT), 0, s, Xte, n_test, d,
-                     w, b, scores, labels, flags);
+  hipLaunchKernelGGL(k_linear_scores<T>, dim3((unsigned)n_test), dim3(NT), 0, s, Xte, d, w, b,
+                     scores, labels, flags);
   return hipGetLastError();
 }
 
