@@ -675,6 +675,27 @@ def test_train_rejects_nonfinite_and_bad_labels(torch_dev):
     assert e.value.code == -2
 
 
+@pytest.mark.parametrize("kernel", ["linear", "rbf"])
+def test_predict_rejects_nonfinite(torch_dev, kernel):
+    """A NaN or an infinity in either point set is reported (ENONFINITE), by the
+    tile path and by the linear kernel's weight shortcut alike."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    X = torch.rand(300, 7, dtype=torch.float64, device=dev)
+    alpha = torch.rand(300, dtype=torch.float64, device=dev) - 0.5
+    Xt = torch.rand(50, 7, dtype=torch.float64, device=dev)
+    kw = dict(kernel=kernel, gamma=0.5)
+    scores, _ = P.predict(X, alpha, 0.1, Xt, **kw)
+    assert bool(torch.isfinite(scores).all())
+    for bad_train in (True, False):
+        for val in (float("nan"), float("inf")):
+            A, B = X.clone(), Xt.clone()
+            (A if bad_train else B)[3, 2] = val
+            with pytest.raises(P.LssvmError) as e:
+                P.predict(A, alpha, 0.1, B, **kw)
+            assert e.value.code == -2, (bad_train, val)
+
+
 def test_train_deterministic(torch_dev):
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
