@@ -696,6 +696,20 @@ def test_predict_rejects_nonfinite(torch_dev, kernel):
             assert e.value.code == -2, (bad_train, val)
 
 
+def test_matvec_rejects_nonfinite(torch_dev):
+    """The product entry point checks its points like training does."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    X = torch.rand(200, 5, dtype=torch.float32, device=dev)
+    p = torch.rand(199, dtype=torch.float32, device=dev)
+    assert bool(torch.isfinite(P.matvec(X, p, kernel="poly", gamma=0.2, coef0=1.0,
+                                        degree=2)).all())
+    X[17, 4] = float("nan")
+    with pytest.raises(P.LssvmError) as e:
+        P.matvec(X, p, kernel="poly", gamma=0.2, coef0=1.0, degree=2)
+    assert e.value.code == -2
+
+
 def test_train_deterministic(torch_dev):
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
