@@ -513,6 +513,36 @@ def test_train_residual_replacement(torch_dev):
     assert res.n_matvec == res.iterations + res.iterations // 50
 
 
+@pytest.mark.parametrize("kernel,dtype,n,d", [("rbf", "f64", 60000, 24), ("linear", "f64", 90000, 16)])
+def test_train_large_kkt_rows(torch_dev, kernel, dtype, n, d):
+    """Training at a size the oracle cannot solve: rows of the full system,
+    f(x_i) + alpha_i / C = y_i (Eq. (11); f evaluated by the oracle from the
+    GPU's alpha and b), hold on 64 sampled points within the CG residual the
+    run reports, and sum(alpha) = 0. fp64: there the kernel values of the two
+    sides agree to rounding, so the CG residual is what bounds each row."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg(kernel, dtype, n, d, C=1.0, eps=1e-8)
+    log(f"train large {cfg.name}")
+    X, y, _ = S.make_train(cfg)
+    r = P.train(to_dev(torch, dev, X), to_dev(torch, dev, y), C=cfg.C, eps=cfg.eps,
+                true_residual=True, **kw_of(cfg))
+    assert r.converged and r.true_rel_residual <= 2 * cfg.eps
+    alpha = r.alpha.cpu().numpy().astype(np.float64)
+    rows = np.unique(np.concatenate([[0, n - 1],
+                                     np.random.default_rng(n).choice(n, 62, replace=False)]))
+    f = O.decision(X, alpha, r.b, X[rows], spec_of(cfg))
+    kkt = f + alpha[rows] / cfg.C - y[rows].astype(np.float64)
+    # every row's residual is bounded by the reduced residual's 2-norm (Eq. (13)
+    # is the full system with the pivot row eliminated), plus the rounding of
+    # alpha to the working precision in the evaluation
+    rhs_norm = float(np.linalg.norm(y[:-1].astype(np.float64) - float(y[-1])))
+    u = 1e-13   # generous for fp64 sums of n terms
+    bound = 2 * r.true_rel_residual * rhs_norm + u * n * max(1.0, float(np.abs(alpha).max()))
+    assert float(np.abs(kkt).max()) <= bound, (float(np.abs(kkt).max()), bound)
+    assert abs(float(alpha.sum())) <= u * n * max(1.0, float(np.abs(alpha).max()))
+
+
 def test_train_matvec_times(torch_dev):
     """Per-product times: one entry per timed product (the residual refresh
     after 50 iterations included), each positive, summing to the reported
