@@ -30,6 +30,15 @@ design notes of the repository):
   residual eps, Sec. IV-B and IV-F) or, unconverged, after max_iter
   iterations (default N); the residual is recomputed as rhs - Q~ x every
   50th iteration (Shewchuk's recommendation);
+* an eps below what the arithmetic can reach ends CG early: at each of those
+  recomputations either the true residual or the CG energy
+  phi(x) = x^T Q~ x / 2 - rhs^T x (which CG lowers at every step in exact
+  arithmetic) must set a new minimum, else CG stops, unconverged, with the
+  iterate of the smallest recomputed residual (Sec. III-B names only "a
+  variant of Shewchuk"; Sec. IV-F shows such a floor);
+* CG stops on curvature breakdown, d^T Q~ d <= 0 or a non-finite step (Q~ is
+  SPD for every kernel of Sec. II-E with coef0 >= 0; a negative coef0 can make
+  it indefinite), with the iterate before that step;
 * the decision label is +1 iff f(x) > 0.
 
 Pins (see tests/test_oracle_pins.py): every function here is checked against
@@ -260,10 +269,12 @@ class CGResult:
     x: np.ndarray
     iterations: int
     converged: bool
-    rel_residual: float          # sqrt(delta / delta0) from the recurrence
+    rel_residual: float          # sqrt(delta / delta0) (recurrence; a true one on a stall)
     true_rel_residual: float     # ||rhs - Q~ x|| / ||rhs||
     n_matvec: int
     history: list                # delta after every iteration
+    stalled: bool = False        # stopped: no new minimum of the true residual
+    breakdown: bool = False      # stopped: d^T Q~ d <= 0 or a non-finite step
 
 
 def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
@@ -274,6 +285,20 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
     q = A d; alpha = delta / d^T q; x += alpha d; r -= alpha q (or r = b - A x
     every ``replace_every`` iterations); delta_new = r^T r; stop once
     delta_new <= eps^2 delta_0; beta = delta_new / delta_old; d = r + beta d.
+
+    Two more ways to stop, both unconverged:
+    * stagnation: at every recomputed residual (a true residual) that has not
+      met eps, progress is a new minimum of either delta_new = r^T r or the
+      energy phi = x^T A x / 2 - b^T x = -(b + r)^T x / 2 over the start and
+      the earlier recomputations. Without progress x returns to the iterate of
+      the smallest recomputed delta. In exact arithmetic phi falls at every
+      step (by (r^T r)^2 / (2 d^T A d)), so it vouches for progress while the
+      residual norm still swings; once phi's changes are below its rounding
+      (near eps ~ sqrt(u)) the residual has to fall. At a floor of the
+      arithmetic neither does, and CG ends a few recomputations later.
+    * breakdown: d^T q <= 0 or a non-finite alpha (an indefinite operator);
+      x is the iterate before that step and ``iterations`` counts the step
+      that found it.
 
     x0 (optional) is a starting iterate: r = b - A x0 (one product). delta_0
     stays b^T b, so the stop test is relative to the right-hand side wherever
@@ -299,15 +324,23 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
     if delta <= eps * eps * delta0:
         true_res = float(np.linalg.norm(b - matvec(x)) / np.linalg.norm(b))
         return CGResult(x, 0, True, float(np.sqrt(delta / delta0)), true_res, nmv, hist)
-    converged = False
+    best_delta, best_x = delta, x.copy()    # the start's residual is a true one
+    best_phi = -0.5 * float((b + r) @ x)
+    converged = stalled = broke = False
     it = 0
     while it < max_iter:
         it += 1
         q = matvec(d)
         nmv += 1
-        alpha = delta / float(d @ q)
+        curv = float(d @ q)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            alpha = float(np.float64(delta) / np.float64(curv))
+        if not (curv > 0.0) or not np.isfinite(alpha):
+            broke = True
+            break
         x += alpha * d
-        if it % replace_every == 0:
+        refresh = it % replace_every == 0
+        if refresh:
             r = b - matvec(x)
             nmv += 1
         else:
@@ -318,16 +351,32 @@ def solve_cg(matvec, rhs, eps: float, max_iter: int = 0,
         if delta <= eps * eps * delta0:
             converged = True
             break
+        if refresh:
+            phi = -0.5 * float((b + r) @ x)
+            progress = False
+            if delta < best_delta:
+                best_delta, best_x = delta, x.copy()
+                progress = True
+            if phi < best_phi:
+                best_phi = phi
+                progress = True
+            if not progress:
+                stalled = True
+                x, delta = best_x, best_delta
+                break
         d = r + (delta / delta_old) * d
     true_res = float(np.linalg.norm(b - matvec(x)) / np.linalg.norm(b))
-    return CGResult(x, it, converged, float(np.sqrt(delta / delta0)), true_res, nmv, hist)
+    return CGResult(x, it, converged, float(np.sqrt(delta / delta0)), true_res, nmv, hist,
+                    stalled, broke)
 
 
 def cg_step(x, r, d, q, rr):
     """One CG iteration given q = A d (Sec. III-B, the steps of solve_cg without
     the product and the stop test): returns x, r, d, r^T r, d^T q, step, beta.
     On curvature breakdown (d^T q <= 0 or a non-finite step) the vectors are
-    returned unchanged with r^T r kept and beta = 0."""
+    returned unchanged with r^T r kept and beta = 0. At an exact solution
+    (rr = 0 on entry, so r = 0) the ratio defining beta is 0 / 0; beta is taken
+    as 0, which restarts the direction at r."""
     x, r, d, q = (_f64(v).copy() for v in (x, r, d, q))
     gamma = float(d @ q)
     with np.errstate(divide="ignore", invalid="ignore"):
@@ -337,7 +386,7 @@ def cg_step(x, r, d, q, rr):
     x += step * d
     r -= step * q
     rr_new = float(r @ r)
-    beta = rr_new / rr
+    beta = rr_new / rr if rr != 0.0 else 0.0
     d = r + beta * d
     return x, r, d, rr_new, gamma, step, beta
 

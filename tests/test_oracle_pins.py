@@ -400,12 +400,92 @@ def test_cg_residual_replacement_and_max_iter():
 
 
 def test_cg_runs_to_max_iter_without_progress():
-    """An affine (not linear) operator keeps CG from converging: it ends at max_iter."""
+    """An affine (not linear) operator keeps CG from converging. With the
+    residual never recomputed, nothing but max_iter ends it; with the default
+    recomputation every 50 iterations, the missing progress of the true
+    residual ends it, unconverged, long before."""
     rng = np.random.default_rng(0)
     A = np.diag(np.linspace(1, 10, 30))
     z = rng.standard_normal(30)
-    res = O.solve_cg(lambda v: A @ v + 0.5 * z, np.ones(30), eps=1e-14, max_iter=500)
-    assert not res.converged and res.iterations == 500 and len(res.history) == 500
+    mv = lambda v: A @ v + 0.5 * z  # noqa: E731
+    res = O.solve_cg(mv, np.ones(30), eps=1e-14, max_iter=500, replace_every=10**9)
+    assert not res.converged and not res.stalled and res.iterations == 500
+    assert len(res.history) == 500
+    res = O.solve_cg(mv, np.ones(30), eps=1e-14, max_iter=500)
+    assert not res.converged and res.stalled and res.iterations < 500
+    assert res.iterations % 50 == 0
+
+
+def _fp32_operator(n=200, kappa=1000.0, seed=1):
+    """SPD A with eigenvalues spread evenly over [1, kappa] and a product
+    rounded to float32: the computed true residual b - fl32(A x) cannot fall
+    much below 2^-24 ||A x||, a floor far above eps = 1e-12."""
+    rng = np.random.default_rng(seed)
+    Qm, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    A = (Qm * np.linspace(1.0, kappa, n)) @ Qm.T
+    A = 0.5 * (A + A.T)
+    b = rng.standard_normal(n)
+    return A, b, (lambda v: (A @ v).astype(np.float32).astype(np.float64))
+
+
+def test_cg_stagnation_stops_at_the_attainable_floor():
+    """eps = 1e-12 is out of reach of a float32 product. CG must stop
+    unconverged within a few recomputations of the residual after reaching the
+    floor (here: 50-150 iterations of progress, then at most two recomputations
+    without a new minimum), not run to max_iter, and return the iterate whose
+    recomputed residual was the smallest. kappa = 1000 keeps the recurrence
+    residual from dropping below eps between two recomputations (a faster
+    operator lets the recurrence reach eps first, a false convergence that the
+    stop test on the recurrence cannot see)."""
+    A, b, mv = _fp32_operator()
+    res = O.solve_cg(mv, b, eps=1e-12, max_iter=5000)
+    assert res.stalled and not res.converged and not res.breakdown
+    assert res.iterations % 50 == 0 and 100 <= res.iterations <= 300
+    # the returned iterate sits at the floor: its exact residual is a few 2^-24
+    exact = np.linalg.norm(b - A @ res.x) / np.linalg.norm(b)
+    assert exact <= 1e-6
+    # and it is the best of the recomputed (true) residuals, each of which is
+    # ||b - fl32(A x_k)||^2 at an iterate x_k
+    refreshed = [res.history[k - 1] for k in range(50, res.iterations + 1, 50)]
+    assert res.rel_residual ** 2 * float(b @ b) == pytest.approx(min(refreshed), rel=1e-12)
+    assert res.true_rel_residual == pytest.approx(res.rel_residual, rel=1e-9)
+    assert refreshed[-1] >= min(refreshed[:-1])      # the last one set no new minimum
+
+
+def test_cg_stagnation_rule_leaves_slow_progress_alone():
+    """kappa = 1e4 (eigenvalues spread geometrically), exact arithmetic: ~1000
+    iterations. The true residual after 50 of them is above the initial one
+    (CG's residual norm is not monotone), but the energy has fallen, and every
+    later recomputation sets a new residual minimum: CG must converge as
+    without the stagnation rule."""
+    rng = np.random.default_rng(2)
+    n = 400
+    Qm, _ = np.linalg.qr(rng.standard_normal((n, n)))
+    A = (Qm * np.geomspace(1.0, 1e4, n)) @ Qm.T
+    A = 0.5 * (A + A.T)
+    b = rng.standard_normal(n)
+    res = O.solve_cg(lambda v: A @ v, b, eps=1e-10, max_iter=5000)
+    assert res.converged and not res.stalled and res.iterations > 100
+    assert np.linalg.norm(b - A @ res.x) <= 2e-10 * np.linalg.norm(b)
+    assert res.history[49] > float(b @ b)        # the swing the energy vouches for
+    plain = O.solve_cg(lambda v: A @ v, b, eps=1e-10, max_iter=5000, replace_every=10**9)
+    assert abs(plain.iterations - res.iterations) <= 100
+
+
+def test_cg_breakdown_on_an_indefinite_matrix_worked_example():
+    """A = diag(3, 1, -1), b = (1, 1, 1), worked by hand. Iteration 1:
+    d = b, d^T A d = 3, a = 1, x = (1, 1, 1), r = (-2, 0, 2), r^T r = 8,
+    beta = 8/3, d = (2/3, 8/3, 14/3). Iteration 2: d^T A d = (12 + 64 - 196)/9
+    = -120/9 <= 0, so CG stops there with x = (1, 1, 1)."""
+    A = np.diag([3.0, 1.0, -1.0])
+    b = np.ones(3)
+    res = O.solve_cg(lambda v: A @ v, b, eps=1e-12)
+    assert res.breakdown and not res.converged and not res.stalled
+    assert res.iterations == 2
+    np.testing.assert_array_equal(res.x, [1.0, 1.0, 1.0])
+    res = O.solve_cg(lambda v: np.diag([1.0, -1.0]) @ v, np.ones(2), eps=1e-12)
+    assert res.breakdown and res.iterations == 1     # d^T A d = 1 - 1 = 0
+    np.testing.assert_array_equal(res.x, [0.0, 0.0])
 
 
 def test_cg_matches_textbook_on_diagonal():
@@ -501,6 +581,17 @@ def test_cg_step_breakdown_leaves_vectors():
     out = O.cg_step(x, r, np.ones(3), -np.ones(3), 12.0)       # negative curvature
     np.testing.assert_array_equal(out[0], x)
     assert out[4] == -3.0 and out[6] == 0.0
+
+
+def test_cg_step_at_an_exact_solution_stays_finite():
+    """r = 0 on entry (rr = 0): the step is 0 / d^T q = 0, nothing moves, and
+    beta (0 / 0) is taken as 0, so d becomes r = 0 and no NaN appears."""
+    x, d = np.array([1.0, -2.0, 3.0]), np.array([0.5, 0.25, -1.0])
+    out = O.cg_step(x, np.zeros(3), d, 2.0 * d, 0.0)
+    np.testing.assert_array_equal(out[0], x)
+    np.testing.assert_array_equal(out[1], 0.0)
+    np.testing.assert_array_equal(out[2], 0.0)
+    assert out[3] == 0.0 and out[4] == 2.0 * float(d @ d) and out[5] == 0.0 and out[6] == 0.0
 
 
 # ------------------------------------------------------------- warm start ---
