@@ -24,10 +24,14 @@
  * - Points are n x d, row-major (point i's d features contiguous).
  * - All work is enqueued on `stream` (a hipStream_t; NULL = default stream)
  *   and the call returns only after it has finished.
- * - Return value: LSSVM_OK (0), LSSVM_NOT_CONVERGED (1, outputs hold the last
- *   iterate) or a negative error code; on error the outputs are unspecified
- *   and lssvm_last_error() describes the cause. Argument checks run on the
- *   host before any GPU work. No C++ exception crosses this boundary.
+ * - Return value: LSSVM_OK (0), LSSVM_NOT_CONVERGED (1, the outputs hold the
+ *   iterate CG stopped with) or a negative error code, described by
+ *   lssvm_last_error(). On LSSVM_EINVAL, LSSVM_ENONFINITE, LSSVM_EBADLABEL and
+ *   LSSVM_EBREAKDOWN the output arrays and b_out are left untouched (a report
+ *   struct such as lssvm_info still records how far the call got); after
+ *   LSSVM_EHIP, a failed HIP runtime call, their contents are unspecified.
+ *   Argument checks run on the host before any GPU work. No C++ exception
+ *   crosses this boundary.
  * - Calls on one stream are serialised by the caller; calls that share a
  *   workspace must not overlap.
  */
@@ -54,12 +58,22 @@ enum {
 /* Status codes. */
 enum {
     LSSVM_OK = 0,
-    LSSVM_NOT_CONVERGED = 1, /* max_iter reached before eps; outputs = last iterate    */
+    LSSVM_NOT_CONVERGED = 1, /* eps not met: max_iter reached (outputs = last iterate)
+                                or CG stalled (outputs = best recomputed iterate)     */
     LSSVM_EINVAL = -1,       /* bad argument (checked on the host, no GPU work done)  */
     LSSVM_ENONFINITE = -2,   /* X (or X_test) holds a NaN or an infinity              */
     LSSVM_EBADLABEL = -3,    /* a label is not exactly +1 or -1                       */
-    LSSVM_EBREAKDOWN = -4,   /* CG curvature d^T Q~ d <= 0 or not finite              */
+    LSSVM_EBREAKDOWN = -4,   /* CG curvature d^T Q~ d <= 0 or not finite (an indefinite
+                                Q~: polynomial kernel with coef0 < 0)                */
     LSSVM_EHIP = -5          /* a HIP runtime call failed                             */
+};
+
+/* Why CG ended (lssvm_info.stop_reason). */
+enum {
+    LSSVM_STOP_EPS = 0,       /* r^T r <= eps^2 rhs^T rhs (or nothing to solve)         */
+    LSSVM_STOP_MAX_ITER = 1,  /* max_iter iterations without meeting eps               */
+    LSSVM_STOP_STALL = 2,     /* no progress at a residual recomputation (eps too small) */
+    LSSVM_STOP_BREAKDOWN = 3  /* d^T Q~ d <= 0: Q~ is not positive definite             */
 };
 
 /* Kernel parameters (Sec. II-E). gamma: poly and rbf (> 0). coef0: the
@@ -74,9 +88,12 @@ typedef struct lssvm_params {
 /* Training report (host struct). Fields marked "in" are read by the library,
  * all others are written by it. */
 typedef struct lssvm_info {
-    int64_t iterations;            /* CG iterations performed                        */
+    int64_t iterations;            /* CG iterations performed (on LSSVM_EBREAKDOWN: the
+                                      iteration whose curvature was not positive)    */
     int64_t n_matvec;              /* implicit Q~ products (incl. residual refreshes) */
-    double rel_residual;           /* sqrt(r^T r / rhs^T rhs) of the CG recurrence    */
+    double rel_residual;           /* sqrt(r^T r / rhs^T rhs) of the CG recurrence (of
+                                      the returned iterate's true residual if CG
+                                      stalled)                                        */
     double true_rel_residual;      /* ||rhs - Q~ x|| / ||rhs|| if requested, else -1  */
     double t_setup_ms;             /* layout, q-vector, right-hand side               */
     double t_cg_ms;                /* CG loop                                         */
@@ -90,7 +107,7 @@ typedef struct lssvm_info {
     int64_t history_capacity;      /* in: length of residual_history                 */
     int32_t time_matvec;           /* in: nonzero -> time every Q~ product with HIP
                                       events recorded on `stream`                    */
-    int32_t reserved2;
+    int32_t stop_reason;           /* why CG ended: LSSVM_STOP_*                     */
     double t_matvec_ms;            /* sum of the timed Q~ products (tile kernel only) */
     int64_t n_matvec_timed;        /* number of products in t_matvec_ms              */
     double* matvec_times;          /* in: host array or NULL; receives the duration in
@@ -127,9 +144,18 @@ size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32
  *           iterations with alpha~ = x0 (alpha_m and b recomputed).
  * b_out     host, the bias of Eq. (15).
  * info      host, may be NULL.
- * CG details: the residual is recomputed as rhs - Q~ x every 50th iteration;
- * reaching max_iter without meeting eps returns LSSVM_NOT_CONVERGED. n = 1
- * or all labels equal give alpha = 0, b = y_m without iterating.
+ * CG details (Sec. III-B): the residual is recomputed as rhs - Q~ x every
+ * 50th iteration. CG ends
+ *   - converged, once r^T r <= eps^2 rhs^T rhs (LSSVM_OK);
+ *   - at max_iter (LSSVM_NOT_CONVERGED, outputs from the last iterate);
+ *   - stalled, when at a recomputation neither the true residual nor the CG
+ *     energy x^T Q~ x / 2 - rhs^T x is below its smallest value at the start
+ *     and at the earlier recomputations: eps lies below what the arithmetic
+ *     attains (LSSVM_NOT_CONVERGED, outputs from the iterate with the
+ *     smallest recomputed residual);
+ *   - on curvature breakdown, d^T Q~ d <= 0 (LSSVM_EBREAKDOWN, outputs
+ *     untouched; Q~ is positive definite for coef0 >= 0).
+ * n = 1 or all labels equal give alpha = 0, b = y_m without iterating.
  */
 int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtype,
                 int32_t kernel, const lssvm_params* kp, double C, double eps,
@@ -144,6 +170,8 @@ int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtyp
  * X_test     device, n_test x d row-major, dtype, n_test >= 1. Must be finite.
  * scores_out device, n_test values, dtype.
  * labels_out device, n_test int32 values (+1/-1), may be NULL.
+ * A NaN or an infinity in X_train or X_test returns LSSVM_ENONFINITE with
+ * scores_out and labels_out untouched.
  */
 int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, int64_t d,
                   int32_t dtype, int32_t kernel, const lssvm_params* kp,
@@ -182,7 +210,8 @@ size_t lssvm_cg_step_workspace_bytes(int64_t N);
  * scalars    device, 4 doubles: in [0] = rr (r^T r of the current iterate);
  *            out [0] = rr', [1] = gamma, [2] = a, [3] = beta. On curvature
  *            breakdown (gamma <= 0 or a not finite) x, r and d are left as
- *            they were, [0] keeps rr and [3] is 0.
+ *            they were, [0] keeps rr and [3] is 0. At an exact solution
+ *            (rr = 0, so r = 0) beta is 0 and d becomes r.
  * workspace  device, lssvm_cg_step_workspace_bytes(N) bytes, 256-byte aligned;
  *            its contents need not survive between calls.
  * stream     HIP stream (NULL = default). Everything is enqueued; nothing is
@@ -193,6 +222,12 @@ size_t lssvm_cg_step_workspace_bytes(int64_t N);
  */
 int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, double* scalars,
                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Host contexts (a pinned buffer and timing events each) that the library
+ * holds: calls lease one for their duration from a process-wide pool, so the
+ * count is the largest number of calls that ever ran at once, not the number
+ * of threads that ever called. Informational. */
+int64_t lssvm_host_contexts(void);
 
 /* Device workspace of lssvm_mfma_peak (a fixed size). */
 size_t lssvm_mfma_peak_workspace_bytes(void);

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(PKG, "liblssvm.so")
 F64, F32 = 0, 1
 LINEAR, POLY, RBF = 0, 1, 2
 OK, NOT_CONVERGED, EINVAL, ENONFINITE, EBADLABEL, EBREAKDOWN, EHIP = 0, 1, -1, -2, -3, -4, -5
+STOP_EPS, STOP_MAX_ITER, STOP_STALL, STOP_BREAKDOWN = 0, 1, 2, 3
 KERNELS = {"linear": LINEAR, "poly": POLY, "polynomial": POLY, "rbf": RBF}
 STATUS_NAMES = {OK: "OK", NOT_CONVERGED: "NOT_CONVERGED", EINVAL: "EINVAL",
                 ENONFINITE: "ENONFINITE", EBADLABEL: "EBADLABEL", EBREAKDOWN: "EBREAKDOWN",
@@ -35,16 +36,20 @@ class Info(ctypes.Structure):
                 ("warm_start", ctypes.c_int32),
                 ("residual_history", ctypes.POINTER(ctypes.c_double)),
                 ("history_capacity", ctypes.c_int64), ("time_matvec", ctypes.c_int32),
-                ("reserved2", ctypes.c_int32), ("t_matvec_ms", ctypes.c_double),
+                ("stop_reason", ctypes.c_int32), ("t_matvec_ms", ctypes.c_double),
                 ("n_matvec_timed", ctypes.c_int64),
                 ("matvec_times", ctypes.POINTER(ctypes.c_double)),
                 ("matvec_times_capacity", ctypes.c_int64)]
 
 
 class LssvmError(RuntimeError):
-    def __init__(self, code: int, msg: str):
+    """A failed call: ``code`` is the library's status, ``info`` (training only)
+    what the call's report recorded before it failed (iterations, ...)."""
+
+    def __init__(self, code: int, msg: str, info: dict | None = None):
         super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
         self.code = code
+        self.info = info or {}
 
 
 _lib = None
@@ -69,6 +74,7 @@ _SIGS = {
                                     ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "lssvm_cg_step_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
+    "lssvm_host_contexts": (ctypes.c_int64, []),
     "lssvm_cg_step": (ctypes.c_int, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
@@ -130,9 +136,9 @@ def last_error() -> str:
     return lib().lssvm_last_error().decode()
 
 
-def _check(code: int, allow_not_converged: bool = False) -> int:
+def _check(code: int, allow_not_converged: bool = False, info: dict | None = None) -> int:
     if code < 0 or (code == NOT_CONVERGED and not allow_not_converged):
-        raise LssvmError(code, last_error())
+        raise LssvmError(code, last_error(), info)
     return code
 
 
@@ -236,6 +242,7 @@ class TrainResult:
     t_cg_ms: float
     t_total_ms: float
     history: list
+    stalled: bool = False     # NOT_CONVERGED because CG stopped making progress
     t_matvec_ms: float = 0.0
     n_matvec_timed: int = 0
     matvec_times: list = dataclasses.field(default_factory=list)   # ms per timed product
@@ -283,12 +290,15 @@ def train(X, y, kernel: str = "linear", gamma: float = 1.0, coef0: float = 0.0,
                              float(C), float(eps), int(max_iter), _dev_ptr(workspace, "workspace"),
                              _nbytes(workspace), _dev_ptr(alpha, "alpha"), ctypes.byref(b),
                              ctypes.byref(info), _stream(X.device))
-    _check(code, allow_not_converged=not raise_not_converged)
+    _check(code, allow_not_converged=not raise_not_converged,
+           info={"iterations": info.iterations, "n_matvec": info.n_matvec,
+                 "rel_residual": info.rel_residual, "stop_reason": info.stop_reason})
+    stalled = info.stop_reason == STOP_STALL
     return TrainResult(alpha, b.value, code, code == OK, info.iterations, info.n_matvec,
                        info.rel_residual, info.true_rel_residual, info.t_setup_ms, info.t_cg_ms,
                        info.t_total_ms,
                        list(hist[:min(history, info.iterations)]) if hist is not None else [],
-                       info.t_matvec_ms, info.n_matvec_timed,
+                       stalled, info.t_matvec_ms, info.n_matvec_timed,
                        list(times[:min(matvec_times, info.n_matvec_timed)])
                        if times is not None else [])
 
@@ -364,6 +374,11 @@ def cg_step(x, r, d, q, scalars, workspace=None):
                                _dev_ptr(q, "q"), _dev_ptr(scalars, "scalars"),
                                _dev_ptr(workspace, "workspace"), _nbytes(workspace),
                                _stream(x.device)))
+
+
+def host_contexts() -> int:
+    """lssvm_host_contexts: host contexts the library holds."""
+    return int(lib().lssvm_host_contexts())
 
 
 def mfma_peak(dtype, device) -> float:

@@ -9,12 +9,14 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -170,7 +172,8 @@ struct TrainWs {
   T* gpart;     // parked inner products of split tail tiles (inside the part region)
   double* pq;   // per tile panel: sum p_j, then sum q_j p_j (2 nT)
   double *rhs, *x, *r, *dir, *qv;
-  double *bp0, *bp1;
+  double* xbest;   // iterate of the smallest recomputed residual (returned on a stall)
+  double *bp0, *bp1, *bp2;
   double* scal;
   int* flags;
   uint32_t* order;
@@ -200,8 +203,10 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.r = c.take<double>(g.NP);
   w.dir = c.take<double>(g.NP);
   w.qv = c.take<double>(g.NP);
+  w.xbest = c.take<double>(g.NP);
   w.bp0 = c.take<double>(g.nb + 1);
   w.bp1 = c.take<double>(g.nb + 1);
+  w.bp2 = c.take<double>(g.nb + 1);   // energy partials at residual recomputations
   w.scal = c.take<double>(S_COUNT);
   w.flags = c.take<int>(F_COUNT);
   w.order = c.take<uint32_t>(LSSVM_TILE_GROUP > 0 ? tri_count(g.nT) : 0);
@@ -218,6 +223,7 @@ struct PredictWs {
   int* flags;
   double* lin_part;  // linear kernel: partial sums of w over point chunks
   double* lin_w;     // linear kernel: w = sum_i alpha_i x_i
+  double* lin_f;     // linear kernel: <w, x> per test point
   int64_t ld_te, nTc, nTr;
   size_t bytes;
 };
@@ -238,14 +244,22 @@ PredictWs<T> carve_predict(const Geometry& g, int64_t n_test, void* base) {
   w.flags = c.take<int>(F_COUNT);
   w.lin_part = c.take<double>(linear_predict_part_elems(g.n, g.d));
   w.lin_w = c.take<double>(g.d);
+  w.lin_f = c.take<double>(n_test);
   w.bytes = c.off;
   return w;
 }
 
-// Pinned host buffer for the few scalars read back per iteration.
-struct HostScratch {
-  double* p = nullptr;
-  int* flags = nullptr;
+// Host-side state of one call in flight: a pinned buffer for the few
+// scalars read back per batch of CG iterations, and timing events (creating
+// a few hundred events costs more than a small training takes). Calls lease
+// a context from a process-wide pool and return it when they end, so the
+// pool holds as many contexts as calls ever ran at once, however many
+// threads come and go; contexts live until the process ends.
+struct HostCtx {
+  double* p = nullptr;   // 64 doubles, pinned
+  int* flags = nullptr;  // inside p
+  int device = -1;       // device the events belong to
+  std::vector<hipEvent_t> ev;
   hipError_t ensure() {
     if (p) return hipSuccess;
     void* v = nullptr;
@@ -256,16 +270,31 @@ struct HostScratch {
     return hipSuccess;
   }
 };
-thread_local HostScratch g_host;
+std::mutex g_pool_mu;
+std::vector<HostCtx*> g_pool_free;
+std::atomic<int64_t> g_pool_size{0};
+thread_local HostCtx* g_ctx = nullptr;   // the context of this thread's call in flight
 
-// Timing events, created once per thread and device and reused by every later
-// training there (creating a few hundred events costs more than a small
-// training takes).
-struct EventPool {
-  int device = -1;
-  std::vector<hipEvent_t> ev;
+struct CtxLease {
+  HostCtx* prev;
+  CtxLease() : prev(g_ctx) {
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    if (!g_pool_free.empty()) {
+      g_ctx = g_pool_free.back();
+      g_pool_free.pop_back();
+    } else {
+      g_ctx = new HostCtx();
+      ++g_pool_size;
+    }
+  }
+  ~CtxLease() {
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    g_pool_free.push_back(g_ctx);
+    g_ctx = prev;
+  }
+  CtxLease(const CtxLease&) = delete;
+  CtxLease& operator=(const CtxLease&) = delete;
 };
-thread_local EventPool g_events;
 
 // HIP events around each implicit product, recorded on the launch stream.
 // Pairs carry the CG iteration they belong to, so products that ran after
@@ -288,17 +317,18 @@ struct MatvecTimer {
     int device = 0;
     hipError_t r = hipGetDevice(&device);
     if (r != hipSuccess) return r;
-    if (g_events.device != device) {
-      for (hipEvent_t e : g_events.ev) (void)hipEventDestroy(e);
-      g_events.ev.clear();
-      g_events.device = device;
+    HostCtx& c = *g_ctx;
+    if (c.device != device) {
+      for (hipEvent_t e : c.ev) (void)hipEventDestroy(e);
+      c.ev.clear();
+      c.device = device;
     }
-    while (g_events.ev.size() < (size_t)(2 * kPairs)) {
+    while (c.ev.size() < (size_t)(2 * kPairs)) {
       hipEvent_t e = nullptr;
       if ((r = hipEventCreate(&e)) != hipSuccess) return r;
-      g_events.ev.push_back(e);
+      c.ev.push_back(e);
     }
-    ev = g_events.ev.data();
+    ev = c.ev.data();
     return hipSuccess;
   }
   // A batch queues at most 32 iterations of at most two products each, so the
@@ -424,10 +454,10 @@ int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t ker
   LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
                               kp.degree, w.norms, w.q64, w.scal, s));
   if (!check) return LSSVM_OK;
-  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipStreamSynchronize(s));
-  if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+  if (g_ctx->flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
   return LSSVM_OK;
 }
 
@@ -488,7 +518,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   TrainWs<T> w = carve_train<T>(g, nullptr);
   LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
   w = carve_train<T>(g, workspace);
-  LSSVM_HIP(g_host.ensure());
+  LSSVM_HIP(g_ctx->ensure());
 
   if (info) {
     info->iterations = 0;
@@ -498,19 +528,20 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     info->rel_residual = 0.0;
     info->true_rel_residual = -1.0;
     info->t_setup_ms = info->t_cg_ms = info->t_total_ms = 0.0;
+    info->stop_reason = LSSVM_STOP_EPS;
   }
 
   if (n == 1) {  // alpha = [0], b = y_0
     LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
     LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
     LSSVM_HIP(launch_single_point<T>(y, alpha_out, w.scal, w.flags, s));
-    LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int),
+    LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int),
                              hipMemcpyDeviceToHost, s));
-    LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
+    LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
     LSSVM_HIP(hipStreamSynchronize(s));
-    if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
-    if (g_host.flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
-    *b_out = g_host.p[0];
+    if (g_ctx->flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+    if (g_ctx->flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
+    *b_out = g_ctx->p[0];
     if (info) {
       info->rel_residual = 0.0;
       info->true_rel_residual = info->compute_true_residual ? 0.0 : -1.0;
@@ -521,15 +552,15 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
 
   // ---- setup: a1, a2, a3 (one read-back for the input flags and r0^T r0)
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, /*check=*/false));
-  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.r, w.dir, w.bp0, w.flags, s));
+  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.xbest, w.r, w.dir, w.bp0, w.flags, s));
   LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
-  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
-  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
   LSSVM_HIP(hipStreamSynchronize(s));
-  if (g_host.flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
-  if (g_host.flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
-  const double delta0 = g_host.p[0];
+  if (g_ctx->flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+  if (g_ctx->flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
+  const double delta0 = g_ctx->p[0];
   const double t_setup = ms_since(t0);
   MatvecTimer tm;
   LSSVM_HIP(tm.init(info && info->time_matvec, info ? info->matvec_times : nullptr,
@@ -538,16 +569,19 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   // ---- a4 + a5: conjugate gradients
   // Iterations are enqueued in batches (1, 2, 4, ... up to 32) and the status
   // is read once per batch; kernels queued after the stop return at once, so
-  // the iterate is the one of the stopping iteration.
+  // the iterate is the one of the stopping iteration. CG stops on eps, on
+  // curvature breakdown, or stalled: at a residual recomputation neither the
+  // true residual nor the energy set a new minimum (the iterate is then the
+  // one with the smallest recomputed residual).
   const auto t1 = clock_t_::now();
   if (max_iter <= 0) max_iter = g.N;
   int64_t queued = 0, it = 0;
   bool done = delta0 == 0.0;  // all labels equal: alpha~ = 0 solves the system
-  bool broke = false;
+  bool broke = false, stalled = false;
   double delta = delta0;
   int status = LSSVM_OK;
   int64_t batch = 1;
-  double* st = g_host.p;
+  double* st = g_ctx->p;
   int64_t warm_products = 0;
   if (info && info->warm_start && !done) {
     // x0 = the caller's alpha~, r0 = rhs - Q~ x0, dir = r0; the stop threshold
@@ -555,8 +589,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
     LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
     LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
-                                 w.r, w.bp1, w.scal, s));
-    LSSVM_HIP(launch_warm_start(w.bp1, g.nb, w.scal, w.r, w.dir, g.NP, s));
+                                 w.r, w.bp1, w.bp2, w.scal, s));
+    LSSVM_HIP(launch_warm_start(w.bp1, w.bp2, g.nb, w.scal, w.r, w.dir, w.x, w.xbest, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
     LSSVM_HIP(hipStreamSynchronize(s));
@@ -577,21 +611,23 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     for (int64_t b = 0; b < nq; ++b) {
       const int64_t k = ++queued;
       const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
+      const bool refresh = k % kReplaceEvery == 0;
       LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
       LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv,
                                  w.bp0, w.scal, s));
-      if (k % kReplaceEvery == 0) {
+      if (refresh) {
         LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
         LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.x, s, tm, k));
         LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
-                                     w.r, w.bp1, w.scal, s));
+                                     w.r, w.bp1, w.bp2, w.scal, s));
       } else {
         LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
       }
       LSSVM_HIP(launch_cg_direction(w.bp1, g.nb, w.scal, par, k, w.r, w.dir, g.NP, w.hist,
-                                    g.NP + 1, s));
+                                    g.NP + 1, refresh ? k / kReplaceEvery : 0, w.bp2, w.x,
+                                    w.xbest, s));
     }
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
@@ -599,6 +635,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     it = (int64_t)st[ST_ITER];
     done = st[ST_DONE] != 0.0;
     broke = st[ST_BREAK] != 0.0;
+    stalled = st[ST_STALL] != 0.0;
     LSSVM_HIP(tm.harvest(done ? it : queued));
     if (broke) {
       it += 1;   // the update of the next iteration found the curvature
@@ -621,15 +658,42 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     it_prev = it;
     delta_prev = delta;
   }
-  const bool converged = done && !broke;
-  const int64_t nmv = it + it / kReplaceEvery + warm_products;
+  const bool converged = done && !broke && !stalled;
+  // products: one per iteration plus each completed residual recomputation
+  // (a breakdown stops before its iteration's recomputation)
+  const int64_t nmv = it + (broke ? it - 1 : it) / kReplaceEvery + warm_products;
   const double t_cg = ms_since(t1);
-  if (status == LSSVM_OK && !converged) {
+  auto report = [&](double t_total) {
+    if (!info) return;
+    info->iterations = it;
+    info->stop_reason = broke     ? LSSVM_STOP_BREAKDOWN
+                        : stalled ? LSSVM_STOP_STALL
+                        : converged ? LSSVM_STOP_EPS
+                                    : LSSVM_STOP_MAX_ITER;
+    info->rel_residual = delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0;
+    info->n_matvec = nmv;
+    info->t_matvec_ms = tm.total_ms;
+    info->n_matvec_timed = tm.count;
+    info->t_setup_ms = t_setup;
+    info->t_cg_ms = t_cg;
+    info->t_total_ms = t_total;
+  };
+  if (status < 0) {   // breakdown: outputs untouched, the report says how far CG got
+    report(ms_since(t0));
+    return status;
+  }
+  if (stalled) {
+    // the iterate of the smallest recomputed residual, whose r^T r the status reported
+    LSSVM_HIP(hipMemcpyAsync(w.x, w.xbest, g.NP * sizeof(double), hipMemcpyDeviceToDevice, s));
+    status = LSSVM_NOT_CONVERGED;
+    fail(LSSVM_NOT_CONVERGED,
+         "CG stalled after %lld iterations: no new minimum of the true residual or the energy "
+         "(best relative residual %g)", (long long)it, std::sqrt(delta / delta0));
+  } else if (!converged) {
     status = LSSVM_NOT_CONVERGED;
     fail(LSSVM_NOT_CONVERGED, "CG stopped after %lld iterations at relative residual %g",
          (long long)it, std::sqrt(delta / delta0));
   }
-  if (status < 0) return status;
   if (info && info->residual_history && it > 0) {
     const int64_t nh = std::min(std::min(it, info->history_capacity), g.NP + 1);
     if (nh > 0) {
@@ -642,9 +706,9 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
 
   // ---- a6: alpha_m and b
   LSSVM_HIP(launch_bias<T>(w.x, w.q64, g.N, y, w.scal, 1.0 / C, alpha_out, s));
-  LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_B, sizeof(double), hipMemcpyDeviceToHost, s));
   LSSVM_HIP(hipStreamSynchronize(s));
-  *b_out = g_host.p[0];
+  *b_out = g_ctx->p[0];
 
   const double t_total = ms_since(t0);   // the optional true-residual product is not training
   if (log_enabled())
@@ -653,29 +717,20 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
                  "setup %.2f ms, cg %.2f ms, total %.2f ms\n",
                  (long long)n, (long long)d, (long long)it,
                  delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0, t_setup, t_cg, t_total);
-  if (info) {
-    info->iterations = it;
-    info->rel_residual = delta0 > 0.0 ? std::sqrt(delta / delta0) : 0.0;
-    if (info->compute_true_residual) {
-      double tr = 0.0;
-      if (delta0 > 0.0) {
-        LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-        LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N,
-                                       w.rhs, w.bp1, s));
-        LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
-        LSSVM_HIP(hipMemcpyAsync(g_host.p, w.scal + S_TRUE, sizeof(double),
-                                 hipMemcpyDeviceToHost, s));
-        LSSVM_HIP(hipStreamSynchronize(s));
-        tr = std::sqrt(g_host.p[0] / delta0);
-      }
-      info->true_rel_residual = tr;
+  report(t_total);
+  if (info && info->compute_true_residual) {
+    double tr = 0.0;
+    if (delta0 > 0.0) {
+      LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
+      LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
+                                     w.bp1, s));
+      LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
+      LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_TRUE, sizeof(double), hipMemcpyDeviceToHost,
+                               s));
+      LSSVM_HIP(hipStreamSynchronize(s));
+      tr = std::sqrt(g_ctx->p[0] / delta0);
     }
-    info->n_matvec = nmv;
-    info->t_matvec_ms = tm.total_ms;
-    info->n_matvec_timed = tm.count;
-    info->t_setup_ms = t_setup;
-    info->t_cg_ms = t_cg;
-    info->t_total_ms = t_total;
+    info->true_rel_residual = tr;
   }
   return status;
 }
@@ -710,7 +765,7 @@ int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_pa
   TrainWs<T> w = carve_train<T>(g, nullptr);
   LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
   w = carve_train<T>(g, workspace);
-  LSSVM_HIP(g_host.ensure());
+  LSSVM_HIP(g_ctx->ensure());
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
   LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, s));
   LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.dir, s));
@@ -727,15 +782,15 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   PredictWs<T> w = carve_predict<T>(g, n_test, nullptr);
   LSSVM_TRY(check_workspace(workspace, ws_bytes, w.bytes));
   w = carve_predict<T>(g, n_test, workspace);
-  LSSVM_HIP(g_host.ensure());
+  LSSVM_HIP(g_ctx->ensure());
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
   if (kernel == LSSVM_LINEAR) {  // Eq. (15): w = sum_i alpha_i x_i, f(x) = <w, x> + b
     LSSVM_HIP(launch_linear_predict<T>(Xtr, alpha, n, d, Xte, n_test, b, w.lin_part, w.lin_w,
-                                       scores, labels, w.flags, s));
-    LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+                                       w.lin_f, scores, labels, w.flags, s));
+    LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                              s));
     LSSVM_HIP(hipStreamSynchronize(s));
-    if (g_host.flags[F_NONFINITE])
+    if (g_ctx->flags[F_NONFINITE])
       return fail(LSSVM_ENONFINITE, "X_train or X_test holds a NaN or an infinity");
     return LSSVM_OK;
   }
@@ -766,11 +821,12 @@ int predict_impl(const T* Xtr, const T* alpha, double b, int64_t n, int64_t d, i
   a.part = w.part;
   a.part_ld = w.ld_te;
   LSSVM_HIP(launch_tiles_gen<T>(a, kernel, w.nTr, s));
-  LSSVM_HIP(launch_predict_finish<T>(w.part, w.nTc, w.ld_te, n_test, b, scores, labels, s));
-  LSSVM_HIP(hipMemcpyAsync(g_host.flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
+  LSSVM_HIP(launch_predict_finish<T>(w.part, w.nTc, w.ld_te, n_test, b, scores, labels, w.flags,
+                                     s));
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
   LSSVM_HIP(hipStreamSynchronize(s));
-  if (g_host.flags[F_NONFINITE])
+  if (g_ctx->flags[F_NONFINITE])
     return fail(LSSVM_ENONFINITE, "X_train or X_test holds a NaN or an infinity");
   return LSSVM_OK;
 }
@@ -825,6 +881,8 @@ int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, d
   }
 }
 
+int64_t lssvm_host_contexts(void) { return g_pool_size.load(); }
+
 size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype) {
   if (n < 1 || d < 1 || !valid_dtype(dtype)) return 0;
   return dtype == LSSVM_F64 ? train_bytes<double>(n, d) : train_bytes<float>(n, d);
@@ -871,6 +929,7 @@ int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtyp
       return fail(LSSVM_EINVAL, "matvec_times_capacity without matvec_times");
     const lssvm_params p = params_or_default(kp);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    CtxLease lease;
     if (dtype == LSSVM_F64)
       return train_impl<double>(static_cast<const double*>(X), static_cast<const double*>(y), n, d,
                                 kernel, p, C, eps, max_iter, workspace, workspace_bytes,
@@ -899,6 +958,7 @@ int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, i
     if (!std::isfinite(b)) return fail(LSSVM_EINVAL, "b must be finite");
     const lssvm_params p = params_or_default(kp);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    CtxLease lease;
     if (dtype == LSSVM_F64)
       return predict_impl<double>(static_cast<const double*>(X_train),
                                   static_cast<const double*>(alpha), b, n, d, kernel, p,
@@ -926,6 +986,7 @@ int lssvm_matvec(const void* X, int64_t n, int64_t d, int32_t dtype, int32_t ker
     if (!(C > 0.0) || !std::isfinite(C)) return fail(LSSVM_EINVAL, "C must be finite and > 0");
     const lssvm_params pr = params_or_default(kp);
     hipStream_t s = static_cast<hipStream_t>(stream);
+    CtxLease lease;
     if (dtype == LSSVM_F64)
       return matvec_impl<double>(static_cast<const double*>(X), n, d, kernel, pr, C,
                                  static_cast<const double*>(p), static_cast<double*>(out),

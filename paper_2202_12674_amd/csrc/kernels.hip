@@ -178,8 +178,8 @@ __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64
 // ------------------------------------------------------------- a3 rhs -------
 template <typename T>
 __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64_t N, int64_t NP,
-                                                  double* rhs, double* x, double* r, double* dir,
-                                                  double* bpart, int* flags) {
+                                                  double* rhs, double* x, double* xbest, double* r,
+                                                  double* dir, double* bpart, int* flags) {
   __shared__ double sh[NT / 64];
   const double ym = (double)y[N];
   if (blockIdx.x == 0 && threadIdx.x == 0 && !(ym == 1.0 || ym == -1.0)) flags[F_BADLABEL] = 1;
@@ -193,6 +193,7 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
     }
     rhs[i] = v;
     x[i] = 0.0;
+    xbest[i] = 0.0;
     r[i] = v;
     dir[i] = v;
     acc += v * v;
@@ -216,6 +217,9 @@ __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int6
     st[ST_DONE] = s == 0.0 ? 1.0 : 0.0;   // all labels equal: alpha~ = 0 solves it
     st[ST_BREAK] = 0.0;
     st[ST_STOP] = eps2 * s;
+    st[ST_STALL] = 0.0;
+    scal[S_BEST] = s;     // x = 0: the residual is rhs, the energy 0
+    scal[S_PHI] = 0.0;
   }
 }
 
@@ -289,12 +293,13 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
 __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part, RankOne c,
                                                      int64_t NP, int64_t N,
                                                      const double* __restrict__ rhs, double* r,
-                                                     double* bp_out, const double* scal) {
+                                                     double* bp_out, double* bp_phi,
+                                                     const double* scal) {
   __shared__ double sh[NT / 64];
   __shared__ double rs[NT];
   if (scal[S_STATUS + ST_DONE] != 0.0) return;
   const RankOneSums ro = rank_one_sums(c, sh);
-  double v = 0.0;
+  double v = 0.0, e = 0.0;
   for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
        r0 += (int64_t)gridDim.x * kRowsPerBlock) {
     const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
@@ -303,9 +308,14 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
     const double ri = i < N ? rhs[i] - qtilde_row(c, ro, i, t) : 0.0;
     r[i] = ri;
     v += ri * ri;
+    e += (rhs[i] + ri) * c.p[i];   // (rhs + r)^T x = -2 x (energy), zero beyond N
   }
   const double t = block_sum(v, sh);
-  if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+  const double u = block_sum(e, sh);
+  if (threadIdx.x == 0) {
+    bp_out[blockIdx.x] = t;
+    bp_phi[blockIdx.x] = u;
+  }
 }
 
 // ||rhs - Q~ x||^2 partials without touching r (final report only).
@@ -329,45 +339,90 @@ __global__ __launch_bounds__(256) void k_true_residual(const double* __restrict_
   if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
 }
 
-// beta = r^T r (new) / r^T r (old); d = r + beta d. Block 0 records the
-// iteration in the status (and the history) and raises done once
-// r^T r <= eps^2 r0^T r0.
+// beta = r^T r (new) / r^T r (old); d = r + beta d (beta = 0 if the old
+// r^T r is 0, an exact solution). Block 0 records the iteration in the
+// status (and the history) and raises done once r^T r <= eps^2 r0^T r0.
+//
+// At the refresh-th residual recomputation (refresh > 0) r is a true
+// residual. Unless it met eps, CG has progressed if r^T r or the energy
+// -(rhs + r)^T x / 2 is below the smallest so far (start and earlier
+// recomputations, kept in slot (refresh - 1) & 1 of S_BEST / S_PHI; the
+// updated minima go to the other slot, so no block reads a slot that block 0
+// writes). A new smallest r^T r copies x to xbest; no progress at all stops
+// CG, stalled, and the status then reports the best r^T r, whose iterate is
+// in xbest.
 __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__ bp_in, int64_t nb,
                                                       double* scal, int par, int64_t iter,
                                                       const double* __restrict__ r, double* dir,
-                                                      int64_t NP, double* hist, int64_t hist_cap) {
+                                                      int64_t NP, double* hist, int64_t hist_cap,
+                                                      int64_t refresh,
+                                                      const double* __restrict__ bp_phi,
+                                                      const double* __restrict__ x,
+                                                      double* __restrict__ xbest) {
   __shared__ double sh[NT / 64];
   double* st = scal + S_STATUS;
   if (st[ST_DONE] != 0.0) return;
   const double dnew = sum_partials(bp_in, nb, sh);
   const double dold = scal[S_DHIST + par];
-  const double beta = dnew / dold;
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
-    dir[i] = r[i] + beta * dir[i];
+  const bool conv = dnew <= st[ST_STOP];
+  bool stall = false;
+  double dbest = dnew;
+  if (refresh > 0 && !conv) {   // uniform over the grid: every block sums the same partials
+    const double phi = -0.5 * sum_partials(bp_phi, nb, sh);
+    const int rd = (int)((refresh - 1) & 1), wr = rd ^ 1;
+    const double bd = scal[S_BEST + rd], bphi = scal[S_PHI + rd];
+    const bool lower_res = dnew < bd, lower_phi = phi < bphi;
+    stall = !lower_res && !lower_phi;
+    dbest = lower_res ? dnew : bd;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      scal[S_BEST + wr] = dbest;
+      scal[S_PHI + wr] = lower_phi ? phi : bphi;
+    }
+    if (lower_res)
+      for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP;
+           i += (int64_t)gridDim.x * NT)
+        xbest[i] = x[i];
+  }
+  const double beta = dold != 0.0 ? dnew / dold : 0.0;
+  if (!stall)
+    for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
+      dir[i] = r[i] + beta * dir[i];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_DHIST + (par ^ 1)] = dnew;
-    st[ST_DELTA] = dnew;
+    st[ST_DELTA] = stall ? dbest : dnew;
     st[ST_CURV] = scal[S_GAMMA];
     st[ST_STEP] = scal[S_ALPHA];
     st[ST_ITER] = (double)iter;
     if (iter <= hist_cap) hist[iter - 1] = dnew;
-    if (dnew <= st[ST_STOP]) st[ST_DONE] = 1.0;
+    if (conv) st[ST_DONE] = 1.0;
+    if (stall) {
+      st[ST_STALL] = 1.0;
+      st[ST_DONE] = 1.0;
+    }
   }
 }
 
 // After r = rhs - Q~ x0 for a warm start: r^T r becomes the current delta
-// (the stop threshold stays eps^2 rhs^T rhs), the direction starts at r, and
-// done is raised if x0 already meets the threshold.
-__global__ __launch_bounds__(256) void k_warm_start(const double* __restrict__ bp_in, int64_t nb,
+// (the stop threshold stays eps^2 rhs^T rhs), the direction starts at r, x0
+// is the best iterate so far (with its residual and energy), and done is
+// raised if x0 already meets the threshold.
+__global__ __launch_bounds__(256) void k_warm_start(const double* __restrict__ bp_in,
+                                                    const double* __restrict__ bp_phi, int64_t nb,
                                                     double* scal, const double* __restrict__ r,
-                                                    double* dir, int64_t NP) {
+                                                    double* dir, const double* __restrict__ x,
+                                                    double* __restrict__ xbest, int64_t NP) {
   __shared__ double sh[NT / 64];
   const double dlt = sum_partials(bp_in, nb, sh);
-  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
+  const double phi = -0.5 * sum_partials(bp_phi, nb, sh);
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     dir[i] = r[i];
+    xbest[i] = x[i];
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     double* st = scal + S_STATUS;
     scal[S_DHIST + 0] = dlt;
+    scal[S_BEST] = dlt;
+    scal[S_PHI] = phi;
     st[ST_DELTA] = dlt;
     if (dlt <= st[ST_STOP]) st[ST_DONE] = 1.0;
   }
@@ -405,7 +460,7 @@ __global__ void k_step_end(const double* scal, double* scalars) {
     scalars[0] = broke ? rr_old : rr_new;
     scalars[1] = scal[S_GAMMA];
     scalars[2] = scal[S_ALPHA];
-    scalars[3] = broke ? 0.0 : rr_new / rr_old;
+    scalars[3] = broke || rr_old == 0.0 ? 0.0 : rr_new / rr_old;   // rr_old = 0: r = 0, beta 0
   }
 }
 
@@ -438,8 +493,9 @@ __global__ void k_single_point(const T* __restrict__ y, T* __restrict__ alpha_ou
                                int* flags) {
   if (threadIdx.x == 0) {
     const double y0 = (double)y[0];
-    if (!(y0 == 1.0 || y0 == -1.0)) flags[F_BADLABEL] = 1;
-    alpha_out[0] = T(0);
+    const bool bad = !(y0 == 1.0 || y0 == -1.0);
+    if (bad) flags[F_BADLABEL] = 1;
+    if (!bad && flags[F_NONFINITE] == 0) alpha_out[0] = T(0);   // outputs untouched on error
     scal[S_B] = y0;
   }
 }
@@ -487,12 +543,13 @@ __global__ __launch_bounds__(256) void k_linear_w_sum(const double* __restrict__
   w[k] = s;
 }
 
-// One block per test point: f = <w, x> + b (fp64), label +1 iff f > 0.
+// One block per test point: f = <w, x> (fp64) into a workspace vector; the
+// bias, the scores and the labels follow in k_predict_finish once every
+// point has been checked.
 template <typename T>
 __global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte, int64_t d,
                                                        const double* __restrict__ w,
-                                                       double b, T* __restrict__ scores,
-                                                       int32_t* __restrict__ labels,
+                                                       double* __restrict__ f,
                                                        int* __restrict__ flags) {
   __shared__ double sh[NT / 64];
   const int64_t t = blockIdx.x;
@@ -505,11 +562,8 @@ __global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte
     acc += (double)xv * w[k];
   }
   if (bad) flags[F_NONFINITE] = 1;
-  const double f = block_sum(acc, sh) + b;
-  if (threadIdx.x == 0) {
-    scores[t] = (T)f;
-    if (labels) labels[t] = f > 0.0 ? 1 : -1;
-  }
+  const double v = block_sum(acc, sh);
+  if (threadIdx.x == 0) f[t] = v;
 }
 
 // ------------------------------------------------------------ tile order ----
@@ -559,7 +613,9 @@ template <typename T>
 __global__ __launch_bounds__(256) void k_predict_finish(const double* __restrict__ part,
                                                         int64_t nslots, int64_t ld, int64_t n_test,
                                                         double b, T* __restrict__ scores,
-                                                        int32_t* __restrict__ labels) {
+                                                        int32_t* __restrict__ labels,
+                                                        const int* __restrict__ flags) {
+  if (flags[F_NONFINITE] != 0) return;   // outputs untouched on error
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
   if (i < n_test) {
     double s = b;
@@ -676,10 +732,11 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 }
 
 template <typename T>
-hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
-                           double* dir, double* bpart, int* flags, hipStream_t s) {
+hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x,
+                           double* xbest, double* r, double* dir, double* bpart, int* flags,
+                           hipStream_t s) {
   hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs,
-                     x, r, dir, bpart, flags);
+                     x, xbest, r, dir, bpart, flags);
   return hipGetLastError();
 }
 
@@ -705,10 +762,10 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
 }
 
 hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, const double* scal,
-                              hipStream_t s) {
+                              const double* rhs, double* r, double* bp_out, double* bp_phi,
+                              const double* scal, hipStream_t s) {
   hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
-                     rhs, r, bp_out, scal);
+                     rhs, r, bp_out, bp_phi, scal);
   return hipGetLastError();
 }
 
@@ -721,16 +778,19 @@ hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP
 
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
-                               double* hist, int64_t hist_cap, hipStream_t s) {
+                               double* hist, int64_t hist_cap, int64_t refresh,
+                               const double* bp_phi, const double* x, double* xbest,
+                               hipStream_t s) {
   hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb,
-                     scal, par, iter, r, dir, NP, hist, hist_cap);
+                     scal, par, iter, r, dir, NP, hist, hist_cap, refresh, bp_phi, x, xbest);
   return hipGetLastError();
 }
 
-hipError_t launch_warm_start(const double* bp_in, int64_t nb, double* scal, const double* r,
-                             double* dir, int64_t NP, hipStream_t s) {
-  hipLaunchKernelGGL(k_warm_start, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, nb, scal,
-                     r, dir, NP);
+hipError_t launch_warm_start(const double* bp_in, const double* bp_phi, int64_t nb, double* scal,
+                             const double* r, double* dir, const double* x, double* xbest,
+                             int64_t NP, hipStream_t s) {
+  hipLaunchKernelGGL(k_warm_start, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, bp_in, bp_phi,
+                     nb, scal, r, dir, x, xbest, NP);
   return hipGetLastError();
 }
 
@@ -743,7 +803,8 @@ hipError_t launch_cg_step(int64_t N, double* x, double* r, double* d, const doub
   hipLaunchKernelGGL(k_cg_update, dim3((unsigned)nb), dim3(NT), 0, s, 0, bp0, nb, scal, 0, d, q,
                      x, r, bp1, N);
   hipLaunchKernelGGL(k_cg_direction, dim3((unsigned)nb), dim3(NT), 0, s, bp1, nb, scal, 0,
-                     (int64_t)1, r, d, N, (double*)nullptr, (int64_t)0);
+                     (int64_t)1, r, d, N, (double*)nullptr, (int64_t)0, (int64_t)0,
+                     (const double*)nullptr, (const double*)nullptr, (double*)nullptr);
   hipLaunchKernelGGL(k_step_end, dim3(1), dim3(64), 0, s, scal, scalars);
   return hipGetLastError();
 }
@@ -779,9 +840,10 @@ hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64
 
 template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
-                                 double b, T* scores, int32_t* labels, hipStream_t s) {
+                                 double b, T* scores, int32_t* labels, const int* flags,
+                                 hipStream_t s) {
   hipLaunchKernelGGL(k_predict_finish<T>, dim3(blocks_for(n_test)), dim3(NT), 0, s, part, nslots,
-                     ld, n_test, b, scores, labels);
+                     ld, n_test, b, scores, labels, flags);
   return hipGetLastError();
 }
 
@@ -801,8 +863,8 @@ hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int 
 
 template <typename T>
 hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_t d, const T* Xte,
-                                 int64_t n_test, double b, double* part, double* w, T* scores,
-                                 int32_t* labels, int* flags, hipStream_t s) {
+                                 int64_t n_test, double b, double* part, double* w, double* f,
+                                 T* scores, int32_t* labels, int* flags, hipStream_t s) {
   const int64_t rows = lin_rows(n);
   const int64_t nchunks = (n + rows - 1) / rows;
   const unsigned gx = (unsigned)((d + NT - 1) / NT);
@@ -813,9 +875,11 @@ hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_
   hipLaunchKernelGGL(k_linear_w_sum, dim3(gx), dim3(NT), 0, s, part, nchunks, d, w);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_linear_scores<T>, dim3((unsigned)n_test), dim3(NT), 0, s, Xte, d, w, b,
-                     scores, labels, flags);
-  return hipGetLastError();
+  hipLaunchKernelGGL(k_linear_scores<T>, dim3((unsigned)n_test), dim3(NT), 0, s, Xte, d, w, f,
+                     flags);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_predict_finish<T>(f, 1, n_test, n_test, b, scores, labels, flags, s);
 }
 
 int64_t linear_predict_part_elems(int64_t n, int64_t d) {
@@ -832,7 +896,7 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
   template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int, int64_t, hipStream_t);    \
   template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
   template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
-                                         double*, double*, int*, hipStream_t);                    \
+                                         double*, double*, double*, int*, hipStream_t);           \
   template hipError_t launch_bias<T>(const double*, const double*, int64_t, const T*, double*,    \
                                      double, T*, hipStream_t);                                    \
   template hipError_t launch_single_point<T>(const T*, T*, double*, int*, hipStream_t);           \
@@ -840,11 +904,11 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
   template hipError_t launch_mv_out<T>(const double*, const RankOne&, int64_t, int64_t, T*,       \
                                        hipStream_t);                                              \
   template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
-                                               T*, int32_t*, hipStream_t);                        \
+                                               T*, int32_t*, const int*, hipStream_t);            \
   template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, hipStream_t);   \
   template hipError_t launch_linear_predict<T>(const T*, const T*, int64_t, int64_t, const T*,    \
-                                               int64_t, double, double*, double*, T*, int32_t*,   \
-                                               int*, hipStream_t);
+                                               int64_t, double, double*, double*, double*, T*,    \
+                                               int32_t*, int*, hipStream_t);
 
 LSSVM_INSTANTIATE(float)
 LSSVM_INSTANTIATE(double)

@@ -29,13 +29,18 @@ enum Scalar : int {
   S_GAMMA = 6,   // curvature d^T Q~ d of the last update
   S_TRUE = 7,    // ||rhs - Q~ x||^2 (final report)
   S_STATUS = 8,  // 8 doubles read by the host after each batch of iterations:
-                 // [0] r^T r of the last iteration run, [1] its curvature,
-                 // [2] its step length, [3] its number, [4] done (converged or
-                 // broken down), [5] breakdown, [6] stop threshold eps^2 r0^T r0
-  S_COUNT = 16
+                 // [0] r^T r of the last iteration run (on a stall: that of the
+                 // best recomputed residual), [1] its curvature, [2] its step
+                 // length, [3] its number, [4] done (converged, broken down or
+                 // stalled), [5] breakdown, [6] stop threshold eps^2 r0^T r0,
+                 // [7] stalled
+  S_BEST = 16,   // smallest true r^T r so far (start, residual recomputations),
+                 // double-buffered by recomputation: [16], [17]
+  S_PHI = 18,    // smallest CG energy -(rhs + r)^T x / 2 so far, likewise: [18], [19]
+  S_COUNT = 24
 };
 enum StatusField : int { ST_DELTA = 0, ST_CURV = 1, ST_STEP = 2, ST_ITER = 3, ST_DONE = 4,
-                         ST_BREAK = 5, ST_STOP = 6, ST_COUNT = 8 };
+                         ST_BREAK = 5, ST_STOP = 6, ST_STALL = 7, ST_COUNT = 8 };
 
 // The CG vector kernels run at most this many blocks of 256 threads (4 per
 // CU), each striding over the vector, so every block can re-sum the previous
@@ -93,8 +98,9 @@ hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t 
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
 template <typename T>
-hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x, double* r,
-                           double* dir, double* bpart, int* flags, hipStream_t s);
+hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x,
+                           double* xbest, double* r, double* dir, double* bpart, int* flags,
+                           hipStream_t s);
 // CG kernels: once the status says done, every later kernel of the queue
 // returns at once, so the host may enqueue iterations ahead of the test.
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
@@ -105,25 +111,37 @@ hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, in
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s);
-// r = rhs - Q~ x (c.p = x) and the block partials of r^T r.
+// r = rhs - Q~ x (c.p = x), the block partials of r^T r and those of
+// (rhs + r)^T x (minus twice the CG energy of x).
 hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, const double* scal,
-                              hipStream_t s);
-// Warm start: delta = r0^T r0 from the block partials, dir = r0, done if
-// already below the stop threshold.
-hipError_t launch_warm_start(const double* bp_in, int64_t nb, double* scal, const double* r,
-                             double* dir, int64_t NP, hipStream_t s);
+                              const double* rhs, double* r, double* bp_out, double* bp_phi,
+                              const double* scal, hipStream_t s);
+// Warm start: delta = r0^T r0 from the block partials, dir = r0, the start as
+// the best iterate so far (its residual and energy), done if already below
+// the stop threshold.
+hipError_t launch_warm_start(const double* bp_in, const double* bp_phi, int64_t nb, double* scal,
+                             const double* r, double* dir, const double* x, double* xbest,
+                             int64_t NP, hipStream_t s);
 // One CG iteration on caller vectors of length N given q = A d: the scalars
 // (device, 4 doubles) carry r^T r in and r^T r, d^T q, step, beta out.
 hipError_t launch_cg_step(int64_t N, double* x, double* r, double* d, const double* q,
                           double* scalars, double* scal, double* bp0, double* bp1,
                           hipStream_t s);
+// beta and the new direction; stop on eps. refresh > 0 marks the refresh-th
+// residual recomputation: then r is a true residual, bp_phi holds the
+// partials of (rhs + r)^T x, and CG stops, stalled, unless the residual or
+// the energy sets a new minimum (x is copied to xbest on a new residual
+// minimum).
 hipError_t launch_cg_direction(const double* bp_in, int64_t nb, double* scal, int par,
                                int64_t iter, const double* r, double* dir, int64_t NP,
-                               double* hist, int64_t hist_cap, hipStream_t s);
+                               double* hist, int64_t hist_cap, int64_t refresh,
+                               const double* bp_phi, const double* x, double* xbest,
+                               hipStream_t s);
 template <typename T>
 hipError_t launch_bias(const double* x, const double* q64, int64_t N, const T* y, double* scal,
                        double invC, T* alpha_out, hipStream_t s);
+// n = 1: alpha = [0] and b = y_0, alpha written only if the point and its
+// label passed the checks (flags set by the layout kernel before it).
 template <typename T>
 hipError_t launch_single_point(const T* y, T* alpha_out, double* scal, int* flags, hipStream_t s);
 template <typename T>
@@ -131,9 +149,12 @@ hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hi
 template <typename T>
 hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
                          hipStream_t s);
+// scores = b + the sum of nslots partial slots; nothing is written if the
+// input flags report a non-finite point.
 template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
-                                 double b, T* scores, int32_t* labels, hipStream_t s);
+                                 double b, T* scores, int32_t* labels, const int* flags,
+                                 hipStream_t s);
 template <typename T>
 hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len_pad,
                              hipStream_t s);
@@ -143,11 +164,12 @@ hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP
                                 const double* rhs, double* bp_out, hipStream_t s);
 
 // Linear-kernel decision values through w = sum_i alpha_i x_i (Eq. (15)).
-// part: linear_predict_part_elems(n, d) doubles; w: d doubles.
+// part: linear_predict_part_elems(n, d) doubles; w: d doubles; f: n_test
+// doubles (the inner products before the bias).
 template <typename T>
 hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_t d, const T* Xte,
-                                 int64_t n_test, double b, double* part, double* w, T* scores,
-                                 int32_t* labels, int* flags, hipStream_t s);
+                                 int64_t n_test, double b, double* part, double* w, double* f,
+                                 T* scores, int32_t* labels, int* flags, hipStream_t s);
 int64_t linear_predict_part_elems(int64_t n, int64_t d);
 
 }  // namespace lssvm

@@ -241,6 +241,10 @@ def test_cg_step_rejects_bad_arguments():
     assert call(wsb=8) == B.EINVAL and "too small" in P.last_error()
 
 
+def test_host_contexts_without_a_call():
+    assert P.lib().lssvm_host_contexts() >= 0
+
+
 def test_mfma_peak_rejects_bad_arguments():
     L = P.lib()
     assert L.lssvm_mfma_peak_workspace_bytes() >= 512 * 256 * 8
