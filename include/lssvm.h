@@ -223,6 +223,24 @@ size_t lssvm_cg_step_workspace_bytes(int64_t N);
 int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, double* scalars,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * lssvm_cg_step without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation. The step works in a fixed array of 32 KiB
+ * of device memory that the library holds on every device it runs on (until
+ * the process ends), which covers every N the call accepts; the call
+ * allocates nothing and writes no memset into the stream.
+ *
+ * Arguments, results and errors as lssvm_cg_step (N in [1, 2^34], else
+ * LSSVM_EINVAL before any GPU work); `stream` must belong to the current
+ * device. Every call on one device shares that device's array, so calls that
+ * may overlap on one device (other streams, other host threads) race and
+ * must be serialised by the caller; each call starts by writing the state it
+ * needs, so nothing carries over from the previous call.
+ */
+int lssvm_cg_step_noalloc(int64_t N, double* x, double* r, double* d, const double* q,
+                          double* scalars, void* stream);
+
 /* Host contexts (a pinned buffer and timing events each) that the library
  * holds: calls lease one for their duration from a process-wide pool, so the
  * count is the largest number of calls that ever ran at once, not the number

@@ -6,11 +6,11 @@ gfx950 matrix cores. The public entry points wrap the C ABI of
 include/lssvm.h; PyTorch supplies device memory and streams only.
 """
 from ._binding import (F32, F64, LINEAR, POLY, RBF, LssvmError, TrainResult,  # noqa: F401
-                       alloc_workspace, cg_step, host_contexts, last_error, lib,
+                       alloc_workspace, cg_step, cg_step_noalloc, host_contexts, last_error, lib,
                        matvec, mfma_peak, predict, predict_workspace_bytes, train,
                        workspace_bytes)
 from .build import LIB_PATH  # noqa: F401
 
-__all__ = ["train", "predict", "matvec", "cg_step", "mfma_peak",
+__all__ = ["train", "predict", "matvec", "cg_step", "cg_step_noalloc", "mfma_peak",
            "workspace_bytes", "predict_workspace_bytes", "alloc_workspace", "host_contexts",
            "LssvmError", "TrainResult", "lib", "last_error"]

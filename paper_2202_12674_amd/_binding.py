@@ -74,6 +74,9 @@ _SIGS = {
                                     ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "lssvm_cg_step_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
+    "lssvm_cg_step_noalloc": (ctypes.c_int, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p]),
     "lssvm_host_contexts": (ctypes.c_int64, []),
     "lssvm_cg_step": (ctypes.c_int, [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -374,6 +377,25 @@ def cg_step(x, r, d, q, scalars, workspace=None):
                                _dev_ptr(q, "q"), _dev_ptr(scalars, "scalars"),
                                _dev_ptr(workspace, "workspace"), _nbytes(workspace),
                                _stream(x.device)))
+
+
+def cg_step_noalloc(x, r, d, q, scalars):
+    """lssvm_cg_step_noalloc: lssvm_cg_step in the library's own fixed device
+    array (no workspace, nothing allocated). Calls on one device must not
+    overlap."""
+    torch = _torch()
+    N = x.numel()
+    for t, nm in ((x, "x"), (r, "r"), (d, "d"), (q, "q"), (scalars, "scalars")):
+        if t.dtype != torch.float64:
+            raise TypeError(f"{nm} must be float64")
+    if not (r.numel() == d.numel() == q.numel() == N) or scalars.numel() < 4:
+        raise ValueError("x, r, d, q need equal lengths and scalars 4 entries")
+    if any(t.device != x.device for t in (r, d, q, scalars)):
+        raise ValueError("x, r, d, q and scalars must be on one device")
+    with torch.cuda.device(x.device):
+        _check(lib().lssvm_cg_step_noalloc(N, _dev_ptr(x, "x"), _dev_ptr(r, "r"),
+                                           _dev_ptr(d, "d"), _dev_ptr(q, "q"),
+                                           _dev_ptr(scalars, "scalars"), _stream(x.device)))
 
 
 def host_contexts() -> int:

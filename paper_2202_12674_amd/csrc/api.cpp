@@ -881,6 +881,34 @@ int lssvm_cg_step(int64_t N, double* x, double* r, double* d, const double* q, d
   }
 }
 
+int lssvm_cg_step_noalloc(int64_t N, double* x, double* r, double* d, const double* q,
+                          double* scalars, void* stream) {
+  try {
+    g_last_error.clear();
+    if (!x || !r || !d || !q || !scalars) return fail(LSSVM_EINVAL, "NULL array argument");
+    if (N < 1 || N > kMaxStepLen)
+      return fail(LSSVM_EINVAL, "N must be in [1, 2^34] (got %lld)", (long long)N);
+    const void* v[4] = {x, r, d, q};
+    for (int i = 0; i < 4; ++i)
+      for (int j = i + 1; j < 4; ++j)
+        if (overlaps(v[i], v[j], N * (int64_t)sizeof(double)))
+          return fail(LSSVM_EINVAL, "x, r, d and q must not overlap");
+    double* base = nullptr;
+    int64_t capacity = 0;
+    LSSVM_HIP(static_scratch(&base, &capacity));
+    const size_t need = carve_step(N, nullptr).bytes;
+    if (need > (size_t)capacity * sizeof(double))
+      return fail(LSSVM_EINVAL, "N = %lld needs %zu bytes of scratch, above the %lld held",
+                  (long long)N, need, (long long)(capacity * (int64_t)sizeof(double)));
+    StepWs w = carve_step(N, base);
+    LSSVM_HIP(launch_cg_step(N, x, r, d, q, scalars, w.scal, w.bp0, w.bp1,
+                             static_cast<hipStream_t>(stream)));
+    return LSSVM_OK;
+  } catch (...) {
+    return fail(LSSVM_EHIP, "internal error");
+  }
+}
+
 int64_t lssvm_host_contexts(void) { return g_pool_size.load(); }
 
 size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype) {

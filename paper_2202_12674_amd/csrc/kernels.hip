@@ -20,6 +20,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 namespace lssvm {
 
@@ -880,6 +881,44 @@ hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_predict_finish<T>(f, 1, n_test, n_test, b, scores, labels, flags, s);
+}
+
+// ------------------------------------------------- static device scratch ----
+// The working memory of lssvm_cg_step_noalloc: the scalar area and the two
+// block-partial arrays of one CG vector step, at most S_COUNT + 2 (1024 + 1)
+// doubles whatever the vector length (the vector kernels run at most
+// kVecBlocks blocks). Every device the library runs on holds one copy until
+// the process ends; calls on one device share it.
+constexpr int64_t kStaticScratchDoubles = 4096;   // 32 KiB
+static_assert(S_COUNT + 2 * (kVecBlocks + 1) + 64 <= kStaticScratchDoubles,
+              "static scratch holds the vector step's scalars and block partials");
+static __device__ __align__(256) double scratch[kStaticScratchDoubles];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[kMaxDevices] = {};   // device address of `scratch`, per device
+}  // namespace
+
+// In host code `scratch` names a host-side stand-in, not device memory: the
+// device address is looked up once per device (with that device current) and
+// only that address is handed to kernels.
+hipError_t static_scratch(double** ptr, int64_t* capacity) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<double*>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
+  *capacity = kStaticScratchDoubles;
+  return hipSuccess;
 }
 
 int64_t linear_predict_part_elems(int64_t n, int64_t d) {

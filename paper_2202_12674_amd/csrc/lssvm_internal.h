@@ -172,4 +172,8 @@ hipError_t launch_linear_predict(const T* Xtr, const T* alpha, int64_t n, int64_
                                  T* scores, int32_t* labels, int* flags, hipStream_t s);
 int64_t linear_predict_part_elems(int64_t n, int64_t d);
 
+// The device array that lssvm_cg_step_noalloc works in, for the current
+// device: its address (resolved once per device) and its size in doubles.
+hipError_t static_scratch(double** ptr, int64_t* capacity);
+
 }  // namespace lssvm

@@ -241,6 +241,20 @@ def test_cg_step_rejects_bad_arguments():
     assert call(wsb=8) == B.EINVAL and "too small" in P.last_error()
 
 
+def test_cg_step_noalloc_rejects_bad_arguments():
+    """The no-workspace step checks its arguments on the host, before it looks
+    up its device array (so these run without a GPU)."""
+    L = P.lib()
+    buf = (ctypes.c_double * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    q = ctypes.c_void_p(ctypes.addressof(buf) + 8 * 16)
+    assert L.lssvm_cg_step_noalloc(0, p, p, p, p, p, None) == -1
+    assert L.lssvm_cg_step_noalloc((1 << 34) + 1, p, p, p, p, p, None) == -1
+    assert L.lssvm_cg_step_noalloc(4, None, p, q, p, p, None) == -1
+    assert L.lssvm_cg_step_noalloc(16, p, q, p, q, p, None) == -1
+    assert "overlap" in P.last_error()
+
+
 def test_host_contexts_without_a_call():
     assert P.lib().lssvm_host_contexts() >= 0
 
