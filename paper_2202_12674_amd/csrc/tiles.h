@@ -174,6 +174,10 @@ __device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
 // Tile rows per band of the general-mode visit order.
 constexpr int64_t kBandRows = 8;
 
+// Third word of a raw buffer resource on gfx9-family targets (32-bit data
+// format, no swizzle, no stride).
+constexpr int kBufferWord3 = 0x00020000;
+
 // Wait until all of this wave's vector memory operations (including direct
 // global -> LDS loads) have completed: s_waitcnt vmcnt(0), other counters free.
 __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -290,7 +294,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     J = r / rows;
     I = band * kBandRows + (r - J * rows);
   }
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is uniform: kept in a scalar register, so the LDS address
+  // of each direct load (M0) needs no per-load read-back from a vector register
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
   // panel I is a.nkb consecutive blocks of BM * BK elements; this workgroup
@@ -298,26 +305,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int64_t nkb = a.nkb / KS;
   const T* __restrict__ Ap = a.A + (I * a.nkb + ks * nkb) * BM * BK;
   const T* __restrict__ Bp = a.B + (J * a.nkb + ks * nkb) * BM * BK;
-  constexpr int64_t astride = (int64_t)BM * BK, bstride = (int64_t)BM * BK;
+  constexpr int64_t astride = (int64_t)BM * BK;   // elements per block of a panel
 
-  // Direct global -> LDS loads of block kb into stage buf: instruction u of
-  // wave w fills physical chunks [(4u + w) * 64, +64) lane by lane; each lane
-  // fetches the logical chunk that belongs at its physical slot.
-  int goff[LOADS];   // element offset of this lane's logical chunk inside a slice
+  // Direct loads of block kb into a stage, memory -> LDS with no registers in
+  // between: instruction u of wave w fills physical chunks [(4u + w) * 64, +64)
+  // lane by lane; each lane fetches the logical chunk that belongs at its
+  // physical slot. They are buffer loads: one buffer resource per panel (scalar
+  // registers, sized to this workgroup's span of the panel, so every load is
+  // in range), the lane's chunk offset as the 32-bit vector offset and the
+  // block's offset as the scalar offset, so a block's loads need no vector
+  // instruction for their addresses. (Global loads into LDS took two 64-bit
+  // vector adds and a readfirstlane per load; at 32768 x 4096 fp32 the tile
+  // kernel ran at 88% of the matrix-core peak with them and 94.5% without,
+  // bit-identical.) The spans stay below 4 GiB (at most 2^21 features: 1 GiB
+  // fp32, 2 GiB fp64 per panel).
+  uint32_t goff[LOADS];
 #pragma unroll
   for (int u = 0; u < LOADS; ++u) {
     const int P = (u * 4 + wave) * 64 + lane;
     const int p = P / CPR, c = (P % CPR) ^ ((p >> 1) & 7);
-    goff[u] = (p * CPR + c) * VEC;
+    goff[u] = (uint32_t)((p * CPR + c) * VEC * (int)sizeof(T));
   }
+  const int span = (int)(uint32_t)((uint64_t)nkb * astride * sizeof(T));
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(Ap), (short)0, span, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rb =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(Bp), (short)0, span, kBufferWord3);
   auto dload = [&](int64_t kb, T (&sa)[CHUNKS * VEC], T (&sb)[CHUNKS * VEC]) {
+    const int so = (int)(uint32_t)((uint64_t)kb * astride * sizeof(T));   // uniform
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int base = (u * 4 + wave) * 64 * VEC;   // wave-uniform LDS element offset
-      __builtin_amdgcn_global_load_lds((gptr_t)(Ap + kb * astride + goff[u]),
-                                       (lptr_t)(&sa[base]), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((gptr_t)(Bp + kb * bstride + goff[u]),
-                                       (lptr_t)(&sb[base]), 16, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lptr_t)(&sa[base]), 16, (int)goff[u], so,
+                                               0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lptr_t)(&sb[base]), 16, (int)goff[u], so,
+                                               0, 0);
     }
   };
 
