@@ -87,6 +87,18 @@ struct Geometry {
   int64_t tail_split;  // ... over this many workgroups each
 };
 
+#ifndef LSSVM_FUSED_SMALL
+#define LSSVM_FUSED_SMALL 1
+#endif
+// Small problems run each CG iteration (except the residual recomputations)
+// as one launch: the product's tiles and, in the last workgroup, the vector
+// work (launch_tiles_cg). Their iterations are launch-bound: four dependent
+// launches of a few microseconds each against a product of ~10 us.
+inline bool fused_iteration(const Geometry& g, int64_t ksplit) {
+  return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP && g.nT * ksplit * g.NP <= kFusedMaxParts &&
+         (ksplit > 1 || g.tail_q == 0);   // one whole-tile launch per product
+}
+
 inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
 
 // Workgroups resident at once in a tile launch: two per CU on 256 CUs.
@@ -178,6 +190,7 @@ struct TrainWs {
   int* flags;
   uint32_t* order;
   double* hist;
+  unsigned* ticket;   // workgroups done in a fused iteration's launch
   size_t bytes;
 };
 
@@ -211,6 +224,7 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.flags = c.take<int>(F_COUNT);
   w.order = c.take<uint32_t>(LSSVM_TILE_GROUP > 0 ? tri_count(g.nT) : 0);
   w.hist = c.take<double>(g.NP + 1);   // r^T r after each iteration (at most N of them)
+  w.ticket = c.take<unsigned>(64);
   w.bytes = c.off;
   return w;
 }
@@ -580,7 +594,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   bool broke = false, stalled = false;
   double delta = delta0;
   int status = LSSVM_OK;
-  int64_t batch = 1;
+  int64_t batch = 1;   // fused (small) problems start at 8, below
   double* st = g_ctx->p;
   int64_t warm_products = 0;
   if (info && info->warm_start && !done) {
@@ -606,12 +620,28 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   // threshold (with a quarter to spare).
   int64_t it_prev = 0, need = max_iter;
   double delta_prev = delta;
+  const bool fused = fused_iteration(g, tile_split(g, kernel));
+  if (fused && !done) LSSVM_HIP(hipMemsetAsync(w.ticket, 0, sizeof(unsigned), s));
+  // A fused iteration takes ~15 us and a status read-back ~30 us: small
+  // problems start with 8 iterations queued (those run past the stop return at
+  // once, a few microseconds each)
+  if (fused) batch = 8;
   while (!done && queued < max_iter) {
     const int64_t nq = std::min<int64_t>(std::min(batch, need), max_iter - queued);
     for (int64_t b = 0; b < nq; ++b) {
       const int64_t k = ++queued;
       const int par = (int)((k - 1) & 1);  // r^T r of the current iterate lives in S_DHIST + par
       const bool refresh = k % kReplaceEvery == 0;
+      if (fused && !refresh) {   // product and vector work in one launch
+        LSSVM_HIP(tm.start(s, k));
+        TileArgs<T> a = sym_args<T>(g, w, kp, kernel, w.dir);
+        a.stop = w.scal + S_STATUS + ST_DONE;
+        FusedCg f{w.ticket, rank_one(g, w, kernel, C, w.dir), w.qv, w.x, w.r, w.dir, w.scal,
+                  w.hist, g.NP, g.N, k, g.NP + 1, par};
+        LSSVM_HIP(launch_tiles_cg<T>(a, kernel, tri_count(g.nT) * a.ksplit, f, s));
+        LSSVM_HIP(tm.stop(s));
+        continue;
+      }
       LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
       LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv,
                                  w.bp0, w.scal, s));

@@ -640,6 +640,94 @@ __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t
   if (threadIdx.x == 0) scal[slot] = s;
 }
 
+// ------------------------------------------------ fused small iteration ----
+// One CG iteration in one launch (launch_tiles_cg): the tiles of q = K d as
+// in k_tiles, then the workgroup that finishes last does what k_cg_gather,
+// k_cg_update and k_cg_direction do, for all rows at once. Each workgroup
+// fences its partial sums (device-scope release) before it takes a ticket;
+// the one that draws the last ticket fences again (acquire) and reads them
+// all. Rows r = tid + 256 k sit in registers (NP <= 1024 -> k < 4).
+template <typename T, int KER>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles_cg(
+    TileArgs<T> a, FusedCg f) {
+  if (!tile_body<T, true, KER, kWhole>(a)) return;   // CG had already stopped
+  __shared__ int last;
+  __shared__ double sh[NT / 64];
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(f.ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+           (unsigned)(a.ntiles - 1);
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  constexpr int R = (int)(kFusedMaxNP / NT);
+  const RankOneSums ro = rank_one_sums(f.c, sh);
+  double qr[R], dr[R];
+  double g = 0.0;
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int64_t i = threadIdx.x + (int64_t)k * NT;
+    qr[k] = dr[k] = 0.0;
+    if (i < f.NP) {
+      double t = 0.0;
+      for (int64_t sl = 0; sl < f.c.nslots; ++sl) t += a.part[sl * f.NP + i];
+      const double q = i < f.N ? qtilde_row(f.c, ro, i, t) : 0.0;
+      qr[k] = q;
+      dr[k] = f.dir[i];
+      f.qv[i] = q;
+      g += dr[k] * q;
+    }
+  }
+  const double gam = block_sum(g, sh);
+  double* st = f.scal + S_STATUS;
+  const double delta = f.scal[S_DHIST + f.par];
+  const double alpha = delta / gam;
+  if (!(gam > 0.0) || !__builtin_isfinite(alpha)) {   // curvature breakdown: nothing moves
+    if (threadIdx.x == 0) {
+      f.scal[S_ALPHA] = alpha;
+      f.scal[S_GAMMA] = gam;
+      st[ST_CURV] = gam;
+      st[ST_STEP] = alpha;
+      st[ST_BREAK] = 1.0;
+      st[ST_DONE] = 1.0;
+      *f.ticket = 0u;
+    }
+    return;
+  }
+  double rr = 0.0, rk[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int64_t i = threadIdx.x + (int64_t)k * NT;
+    rk[k] = 0.0;
+    if (i < f.NP) {
+      f.x[i] += alpha * dr[k];
+      rk[k] = f.r[i] - alpha * qr[k];
+      f.r[i] = rk[k];
+      rr += rk[k] * rk[k];
+    }
+  }
+  const double dnew = block_sum(rr, sh);
+  const double beta = delta != 0.0 ? dnew / delta : 0.0;
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int64_t i = threadIdx.x + (int64_t)k * NT;
+    if (i < f.NP) f.dir[i] = rk[k] + beta * dr[k];
+  }
+  if (threadIdx.x == 0) {
+    f.scal[S_ALPHA] = alpha;
+    f.scal[S_GAMMA] = gam;
+    f.scal[S_DHIST + (f.par ^ 1)] = dnew;
+    st[ST_DELTA] = dnew;
+    st[ST_CURV] = gam;
+    st[ST_STEP] = alpha;
+    st[ST_ITER] = (double)f.iter;
+    if (f.iter <= f.hist_cap) f.hist[f.iter - 1] = dnew;
+    if (dnew <= st[ST_STOP]) st[ST_DONE] = 1.0;
+    *f.ticket = 0u;   // the next launch starts after this one ends
+  }
+}
+
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + NT - 1) / NT); }
 
 }  // namespace
@@ -730,6 +818,27 @@ hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t 
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s) {
   return launch_tiles<T, false, kWhole>(a, kernel, nTr * a.nTc, s);
+}
+
+template <typename T>
+hipError_t launch_tiles_cg(const TileArgs<T>& a0, int kernel, int64_t nwg, const FusedCg& f,
+                           hipStream_t s) {
+  if (nwg > kMaxTileGrid) return hipErrorInvalidValue;   // small problems only: one chunk
+  TileArgs<T> a = a0;
+  a.ntiles = nwg;
+  a.tile_base = 0;
+  switch (kernel) {
+    case KLIN:
+      hipLaunchKernelGGL((k_tiles_cg<T, KLIN>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      break;
+    case KPOLY:
+      hipLaunchKernelGGL((k_tiles_cg<T, KPOLY>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      break;
+    default:
+      hipLaunchKernelGGL((k_tiles_cg<T, KRBF>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      break;
+  }
+  return hipGetLastError();
 }
 
 template <typename T>
@@ -934,6 +1043,8 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
                                         hipStream_t);                                             \
   template hipError_t launch_tiles_sym<T>(const TileArgs<T>&, int, int, int64_t, hipStream_t);    \
   template hipError_t launch_tiles_gen<T>(const TileArgs<T>&, int, int64_t, hipStream_t);         \
+  template hipError_t launch_tiles_cg<T>(const TileArgs<T>&, int, int64_t, const FusedCg&,        \
+                                         hipStream_t);                                            \
   template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
                                          double*, double*, double*, int*, hipStream_t);           \
   template hipError_t launch_bias<T>(const double*, const double*, int64_t, const T*, double*,    \

@@ -79,6 +79,21 @@ struct RankOne {
   double invC;
 };
 
+// One fused CG iteration for small problems (see launch_tiles_cg): the
+// product's tiles, then, in the workgroup that finishes last, the vector work
+// of k_cg_gather, k_cg_update and k_cg_direction on the whole vectors.
+struct FusedCg {
+  unsigned* ticket;   // zero before every launch; the last workgroup resets it
+  RankOne c;          // c.p = the CG direction
+  double *qv, *x, *r, *dir, *scal, *hist;
+  int64_t NP, N, iter, hist_cap;
+  int par;            // r^T r of the current iterate lives in S_DHIST + par
+};
+// Largest padded length and partial-slot count the fused iteration handles:
+// one workgroup reads every partial (NP x nslots doubles) and keeps each
+// thread's rows (NP / 256) in registers.
+constexpr int64_t kFusedMaxNP = 1024, kFusedMaxParts = 1 << 16;
+
 // The symmetric tiles' visit order (GROUP x GROUP super-tiles), packed
 // (I << 16) | J, nT (nT + 1) / 2 entries.
 hipError_t launch_tile_order(int64_t nT, int64_t group, uint32_t* order, hipStream_t s);
@@ -97,6 +112,16 @@ hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t 
                             hipStream_t s);
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
+// A whole CG iteration in one launch for small problems (NP <= kFusedMaxNP,
+// NP x partial slots <= kFusedMaxParts, a single whole-tile launch per
+// product): the symmetric tiles of q = Q~ d, then the workgroup that
+// finishes last (an atomic ticket after a device-scope release fence) adds the
+// rank-one terms and does the update and the new direction, with the same
+// status, stop test and breakdown handling as the separate kernels. Nothing
+// waits on another workgroup.
+template <typename T>
+hipError_t launch_tiles_cg(const TileArgs<T>& a, int kernel, int64_t nwg, const FusedCg& f,
+                           hipStream_t s);
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x,
                            double* xbest, double* r, double* dir, double* bpart, int* flags,

@@ -196,9 +196,11 @@ __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // separate partial slots: kPartial workgroups park their raw inner products
 // G (the accumulators) in a.gpart and stop; a kFixup launch, one workgroup
 // per tile, sums the parked splits in split order and runs the epilogue.
+//
+// The body returns false when the launch found CG already stopped (nothing
+// done), true otherwise.
 template <typename T, bool SYM, int KER, int PART>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles(
-    TileArgs<T> a) {
+__device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   using MF = Mfma<T>;
   using C = TileCfg<T>;
   constexpr int BM = C::BM, BK = C::BK;
@@ -246,7 +248,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ __attribute__((aligned(16))) T vt[3][BM];
 
   if constexpr (SYM) {
-    if (a.stop && *a.stop != 0.0) return;   // CG already stopped
+    if (a.stop && *a.stop != 0.0) return false;   // CG already stopped
   }
   int64_t I, J;
   // Symmetric tiles may have their features split over KS workgroups. For
@@ -466,7 +468,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             for (int e = 0; e < PER; ++e) x[e] = acc[i][j][w * PER + e];
             *unit_ptr(ks, (i * CB + j) * UPB + w) = x;
           }
-      return;
+      return true;
     } else {
       if constexpr (kVecLds) {
         dvec();
@@ -639,6 +641,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       }
     }
   }
+  return true;
+}
+
+template <typename T, bool SYM, int KER, int PART>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles(
+    TileArgs<T> a) {
+  tile_body<T, SYM, KER, PART>(a);
 }
 
 
