@@ -195,6 +195,43 @@ def cpu_phases(cfg, X, y, X_test, n_sub: int):
     return out
 
 
+def cpu_full(cfg, X, y, X_test):
+    """The oracle's time to eps on the whole workload, every phase on the host
+    cores: dense Q~ assembly (BLAS), CG with the explicit Q~ at the workload's
+    eps (the same stop rule as the GPU), the recovery of alpha and b, the
+    Cholesky factor and solve of the same system, and the prediction of the
+    test points. Dense fp64 Q~ of the 32768-point workload is 8 GiB; run it
+    where the host has room (not part of the default run)."""
+    import numpy as np
+    import oracle as O
+    spec = O.KernelSpec(cfg.kernel, gamma=cfg.gamma, coef0=cfg.coef0, degree=cfg.degree)
+    X64, y64 = X.astype(np.float64), y.astype(np.float64)
+    out = {"workload": cfg.name, "host": host_facts()}
+    t0 = time.perf_counter()
+    Qt, q, Qmm = O.reduced_matrix(X64, spec, cfg.C)
+    out["assembly_s"] = round(time.perf_counter() - t0, 3)
+    rhs = O.reduced_rhs(y64)
+    t = time.perf_counter()
+    res = O.solve_cg(lambda v: O.matvec_dense(Qt, v), rhs, cfg.eps, cfg.max_iter)
+    alpha, b = O.recover(res.x, y64, q, Qmm)
+    out["cg_s"] = round(time.perf_counter() - t, 3)
+    out["cg_iterations"] = res.iterations
+    out["cg_s_per_iteration"] = round(out["cg_s"] / max(1, res.n_matvec), 4)
+    out["time_to_eps_s"] = round(out["assembly_s"] + out["cg_s"], 3)
+    t = time.perf_counter()
+    O.solve_cholesky(Qt, rhs)
+    out["cholesky_s"] = round(time.perf_counter() - t, 3)
+    del Qt
+    t = time.perf_counter()
+    O.predict(X64, alpha, b, X_test.astype(np.float64), spec)
+    out["predict_s"] = round(time.perf_counter() - t, 3)
+    # the oracle's CG multiplies by the assembled Q~ (2 N^2 flop, memory-bound);
+    # the assembly is where it forms the kernel values the GPU forms per product
+    N = cfg.n - 1
+    out["dense_product_gflops"] = round(2.0 * N * N / 1e9 / out["cg_s_per_iteration"], 2)
+    return out
+
+
 def device_facts(torch, dev):
     p = torch.cuda.get_device_properties(dev)
     return {"name": p.name, "compute_units": p.multi_processor_count,
@@ -215,6 +252,9 @@ def main():
                     help="vector length of the standalone CG vector-step measurement (0: skip)")
     ap.add_argument("--cpu-phase-points", type=int, default=4096,
                     help="points of the workload for the oracle's per-phase timing (0: skip)")
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="only the oracle's time to eps on the whole workload (host cores; "
+                         "dense Q~ of 8 GiB at the default workload), then exit")
     ap.add_argument("--only-peak", choices=["f32", "f64"],
                     help="only the matrix-core loop peak probe for one dtype (for profiling)")
     ap.add_argument("--only-a5", action="store_true",
@@ -232,6 +272,13 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": args.calibrate_copy << 20, "reps": 3}))
+        return
+    if args.cpu_full:
+        import synthdata as S
+        cfg = S.CONFIGS[args.config]
+        X, y, scale = S.make_train(cfg)
+        Xte, _ = S.make_test(cfg, scale, n_test=args.n_test)
+        print(json.dumps({"cpu_full": cpu_full(cfg, X, y, Xte)}), flush=True)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
