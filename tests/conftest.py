@@ -11,3 +11,15 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    """(torch, cuda:0) for GPU tests; loads the HIP library so that a missing
+    build fails loudly instead of skipping."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2202_12674_amd as P
+    P.lib()
+    return torch, torch.device("cuda:0")
