@@ -95,7 +95,7 @@ struct Geometry {
 // work (launch_tiles_cg). Their iterations are launch-bound: four dependent
 // launches of a few microseconds each against a product of ~10 us.
 inline bool fused_iteration(const Geometry& g, int64_t ksplit) {
-  return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP && g.nT * ksplit * g.NP <= kFusedMaxParts &&
+  return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP &&
          (ksplit > 1 || g.tail_q == 0);   // one whole-tile launch per product
 }
 
@@ -123,7 +123,7 @@ inline int64_t linear_split(int64_t nT, int64_t nkb) {
   double best_cost = cost(1);
   for (int64_t S = 2; S <= LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0; S *= 2) {
     const double c = cost(S);
-    if (c < 0.95 * best_cost) {   // a clear gain only: each split adds partial slots
+    if (c < 0.95 * best_cost) {   // a clear gain only: each split adds workgroups and atomics
       best = S;
       best_cost = c;
     }
@@ -180,8 +180,8 @@ struct TrainWs {
   T* Xt;
   T* norms;
   double* q64;
-  double* part;
-  T* gpart;     // parked inner products of split tail tiles (inside the part region)
+  int64_t* acc; // fixed-point row sums of a product (two words per row)
+  T* gpart;     // parked inner products of split tail tiles
   double* pq;   // per tile panel: sum p_j, then sum q_j p_j (2 nT)
   double *rhs, *x, *r, *dir, *qv;
   double* xbest;   // iterate of the smallest recomputed residual (returned on a stall)
@@ -202,14 +202,10 @@ TrainWs<T> carve_train(const Geometry& g, void* base) {
   w.Xt = c.take<T>(g.d_pad * g.ld);
   w.norms = c.take<T>(g.ld);
   w.q64 = c.take<double>(g.ld);
-  // Tile partials: nT ksplit slots for the linear kernel's split tiles, or nT
-  // slots followed by the parked inner products of the split tail tiles.
-  const int64_t tail_elems = g.tail_q * g.tail_split * g.tile * g.tile;
-  const int64_t slot_bytes = g.nT * g.NP * (int64_t)sizeof(double);
-  const int64_t part_bytes = std::max<int64_t>(slot_bytes * g.ksplit,
-                                               slot_bytes + tail_elems * (int64_t)sizeof(T));
-  w.part = c.take<double>((part_bytes + 7) / 8);
-  w.gpart = w.part ? reinterpret_cast<T*>(reinterpret_cast<char*>(w.part) + slot_bytes) : nullptr;
+  // Row sums: two 64-bit words per row, however many tiles add to them; the
+  // split tail's parked inner products (at most a quarter round of tiles).
+  w.acc = c.take<int64_t>(2 * g.NP);
+  w.gpart = c.take<T>(g.tail_q * g.tail_split * g.tile * g.tile);
   w.pq = c.take<double>(2 * g.nT);
   w.rhs = c.take<double>(g.NP);
   w.x = c.take<double>(g.NP);
@@ -395,7 +391,7 @@ int check_sizes(int64_t n, int64_t d, int64_t min_n) {
   if (n < min_n) return fail(LSSVM_EINVAL, "n must be >= %lld (got %lld)", (long long)min_n,
                              (long long)n);
   if (d < 1) return fail(LSSVM_EINVAL, "d must be >= 1 (got %lld)", (long long)d);
-  // supported range: the tile partials alone take n^2 / 16 bytes (1 TiB at
+  // supported range: the tile visit order takes n^2 / 8192 bytes (2 GiB at
   // n = 2^22), and the tile order packs tile indices in 16 bits
   if (n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
     return fail(LSSVM_EINVAL, "problem too large (n=%lld, d=%lld)", (long long)n, (long long)d);
@@ -443,8 +439,9 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.nTc = g.nT;
   a.ksplit = tile_split(g, kernel);
   a.order = LSSVM_TILE_GROUP > 0 ? w.order : nullptr;
-  a.part = w.part;
-  a.part_ld = g.NP;
+  a.acc = w.acc;
+  a.fx = w.scal + S_PMAX;      // [S_PMAX], [S_NMAX], [S_FIXSC]
+  a.fx_bad = w.flags + F_PRODUCT;
   return a;
 }
 
@@ -464,6 +461,8 @@ int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t ker
                  const lssvm_params& kp, hipStream_t s, bool check = true) {
   LSSVM_TRY(make_order<T>(g, w, s));
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
+  LSSVM_HIP(hipMemsetAsync(w.scal, 0, S_COUNT * sizeof(double), s));
+  LSSVM_HIP(hipMemsetAsync(w.acc, 0, 2 * g.NP * sizeof(int64_t), s));
   LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
                               kp.degree, w.norms, w.q64, w.scal, s));
@@ -475,11 +474,12 @@ int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t ker
   return LSSVM_OK;
 }
 
-// The terms of Q~ p that the tile partials leave out, for the vector p.
+// A finished product's row sums and the terms of Q~ p the tiles leave out.
 template <typename T>
 RankOne rank_one(const Geometry& g, const TrainWs<T>& w, int32_t kernel, double C,
                  const double* p) {
-  return RankOne{w.pq, g.nT, g.nT * tile_split(g, kernel), w.q64, p, w.scal, 1.0 / C};
+  (void)kernel;
+  return RankOne{w.pq, g.nT, w.acc, w.q64, p, w.scal, w.flags, 1.0 / C};
 }
 
 // The tile launches of one product: all tiles whole (the linear kernel's
@@ -566,7 +566,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
 
   // ---- setup: a1, a2, a3 (one read-back for the input flags and r0^T r0)
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, /*check=*/false));
-  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.xbest, w.r, w.dir, w.bp0, w.flags, s));
+  LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.xbest, w.r, w.dir, w.bp0, w.flags,
+                               w.scal, s));
   LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
   LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
                            s));
@@ -600,10 +601,10 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   if (info && info->warm_start && !done) {
     // x0 = the caller's alpha~, r0 = rhs - Q~ x0, dir = r0; the stop threshold
     // set from rhs^T rhs above is kept
-    LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, s));
+    LSSVM_HIP(launch_pad_to_f64<T>(alpha_out, g.N, w.x, g.NP, w.scal, s));
     LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-    LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
-                                 w.r, w.bp1, w.bp2, w.scal, s));
+    LSSVM_HIP(launch_cg_residual(rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
+                                 w.r, w.bp1, w.bp2, s));
     LSSVM_HIP(launch_warm_start(w.bp1, w.bp2, g.nb, w.scal, w.r, w.dir, w.x, w.xbest, g.NP, s));
     LSSVM_HIP(hipMemcpyAsync(st, w.scal + S_STATUS, ST_COUNT * sizeof(double),
                              hipMemcpyDeviceToHost, s));
@@ -643,14 +644,13 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
         continue;
       }
       LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.dir, s, tm, k));
-      LSSVM_HIP(launch_cg_gather(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv,
-                                 w.bp0, w.scal, s));
+      LSSVM_HIP(launch_cg_gather(rank_one(g, w, kernel, C, w.dir), g.NP, g.N, w.qv, w.bp0, s));
       if (refresh) {
         LSSVM_HIP(launch_cg_update(1, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
         LSSVM_TRY(timed_matvec<T>(g, w, kp, kernel, w.x, s, tm, k));
-        LSSVM_HIP(launch_cg_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
-                                     w.r, w.bp1, w.bp2, w.scal, s));
+        LSSVM_HIP(launch_cg_residual(rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
+                                     w.r, w.bp1, w.bp2, s));
       } else {
         LSSVM_HIP(launch_cg_update(0, w.bp0, g.nb, w.scal, par, w.dir, w.qv, w.x, w.r, w.bp1,
                                    g.NP, s));
@@ -752,8 +752,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
     double tr = 0.0;
     if (delta0 > 0.0) {
       LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.x, s));
-      LSSVM_HIP(launch_true_residual(w.part, rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs,
-                                     w.bp1, s));
+      LSSVM_HIP(launch_true_residual(rank_one(g, w, kernel, C, w.x), g.NP, g.N, w.rhs, w.bp1, s));
       LSSVM_HIP(launch_finish_sum(w.bp1, g.nb, w.scal, S_TRUE, s));
       LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_TRUE, sizeof(double), hipMemcpyDeviceToHost,
                                s));
@@ -797,9 +796,9 @@ int matvec_impl(const T* X, int64_t n, int64_t d, int32_t kernel, const lssvm_pa
   w = carve_train<T>(g, workspace);
   LSSVM_HIP(g_ctx->ensure());
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s));
-  LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, s));
+  LSSVM_HIP(launch_pad_to_f64<T>(p, g.N, w.dir, g.NP, w.scal, s));
   LSSVM_TRY(matvec_partials<T>(g, w, kp, kernel, w.dir, s));
-  LSSVM_HIP(launch_mv_out<T>(w.part, rank_one(g, w, kernel, C, w.dir), g.NP, g.N, out, s));
+  LSSVM_HIP(launch_mv_out<T>(rank_one(g, w, kernel, C, w.dir), g.NP, g.N, out, s));
   LSSVM_HIP(hipStreamSynchronize(s));
   return LSSVM_OK;
 }

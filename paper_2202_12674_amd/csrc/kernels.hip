@@ -82,25 +82,44 @@ __device__ inline double qtilde_row(const RankOne& c, const RankOneSums& r, int6
   return kp + (r.qmm - c.q64[i]) * r.S - r.Tq + c.p[i] * c.invC;
 }
 
-// Tile partial sums of rows [r0, r0 + 32): thread (g, r) = (tid / 32, tid % 32)
-// adds slots g, g + 8, g + 16, ... of row r0 + r, then the eight group sums
-// are added in group order through sh (8 x 32 doubles). The total of row
-// r0 + tid lands in threads tid < 32. Fixed order: the same sum every run.
-// Called by every thread of the block.
-__device__ inline double row_slot_sum(const double* __restrict__ part, int64_t nslots, int64_t NP,
-                                      int64_t r0, double* sh) {
-  const int r = threadIdx.x % kRowsPerBlock, g = threadIdx.x / kRowsPerBlock;
-  const int64_t i = r0 + r;
-  double s = 0.0;
-  if (i < NP)
-    for (int64_t sl = g; sl < nslots; sl += kSlotGroups) s += part[sl * NP + i];
-  __syncthreads();   // the previous chunk's reads of sh are done
-  sh[g * kRowsPerBlock + r] = s;
+// Block-wide maximum of one non-negative double per thread; every thread
+// gets it.
+__device__ inline double block_max(double v, double* sh) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   __syncthreads();
-  double t = 0.0;
-  if (g == 0)
-    for (int k = 0; k < kSlotGroups; ++k) t += sh[k * kRowsPerBlock + r];
-  return t;
+  if (l == 0) sh[w] = v;
+  __syncthreads();
+  double m = 0.0;
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) m = fmax(m, sh[i]);
+  return m;
+}
+
+// Raise scal[S_PMAX], the bound on |p_j| that fixes the next product's
+// fixed-point scale, to m >= 0: the bits of non-negative doubles order like
+// their values, so an integer atomic max keeps the largest whatever the order.
+__device__ inline void raise_pmax(double* scal, double m) {
+  atomicMax(reinterpret_cast<unsigned long long*>(scal + S_PMAX),
+            (unsigned long long)__double_as_longlong(m));
+}
+
+// Row i's sum over the product's tiles from its two fixed-point words (see
+// fixed_add in tiles.h): the exact integer sum, rounded once to fp64 and
+// unscaled. The words are cleared for the next product.
+__device__ inline double fixed_take(int64_t* acc, int64_t i, double inv_scale) {
+  const int64_t L = acc[2 * i], H = acc[2 * i + 1];
+  acc[2 * i] = 0;
+  acc[2 * i + 1] = 0;
+  const int64_t H2 = H + (L >> 32);   // L >= 0: a sum of unsigned 32-bit limbs
+  const int64_t L2 = L & 0xffffffffLL;
+  return ((double)H2 * 4294967296.0 + (double)L2) * inv_scale;
+}
+
+// (K p)_i of a finished product, or NaN once any of its row sums was not finite.
+__device__ inline double product_row(const RankOne& c, int64_t i, double inv_scale, bool bad) {
+  const double t = fixed_take(c.acc, i, inv_scale);
+  return bad ? __builtin_nan("") : t;
 }
 
 // ------------------------------------------------------------- a1 layout ----
@@ -142,37 +161,46 @@ __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64
                                                  double coef0, int degree, T* __restrict__ norms,
                                                  double* __restrict__ q64,
                                                  double* __restrict__ scal) {
+  __shared__ double sh[NT / 64];
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i >= ld) return;
-  double nrm = 0.0, dot = 0.0, dist = 0.0;
-  const T* pi = Xb + ((i / TP) * nkb * TP + i % TP) * BK;   // point i, block 0
-  const T* pm = m >= 0 ? Xb + ((m / TP) * nkb * TP + m % TP) * BK : pi;   // pivot, block 0
-  for (int64_t kb = 0; kb < nkb; ++kb) {
-    const T* xi = pi + kb * TP * BK;            // this point's BK features (padding is 0)
-    if (m >= 0) {
-      const T* xm = pm + kb * TP * BK;
+  double nrm = 0.0;
+  if (i < ld) {
+    double dot = 0.0, dist = 0.0;
+    const T* pi = Xb + ((i / TP) * nkb * TP + i % TP) * BK;   // point i, block 0
+    const T* pm = m >= 0 ? Xb + ((m / TP) * nkb * TP + m % TP) * BK : pi;   // pivot, block 0
+    for (int64_t kb = 0; kb < nkb; ++kb) {
+      const T* xi = pi + kb * TP * BK;            // this point's BK features (padding is 0)
+      if (m >= 0) {
+        const T* xm = pm + kb * TP * BK;
 #pragma unroll
-      for (int kk = 0; kk < BK; ++kk) {
-        const double xv = (double)xi[kk], xw = (double)xm[kk];
-        nrm += xv * xv;
-        dot += xv * xw;
-        const double df = xv - xw;
-        dist += df * df;
-      }
-    } else {
+        for (int kk = 0; kk < BK; ++kk) {
+          const double xv = (double)xi[kk], xw = (double)xm[kk];
+          nrm += xv * xv;
+          dot += xv * xw;
+          const double df = xv - xw;
+          dist += df * df;
+        }
+      } else {
 #pragma unroll
-      for (int kk = 0; kk < BK; ++kk) {
-        const double xv = (double)xi[kk];
-        nrm += xv * xv;
+        for (int kk = 0; kk < BK; ++kk) {
+          const double xv = (double)xi[kk];
+          nrm += xv * xv;
+        }
       }
     }
+    norms[i] = (T)nrm;
+    if (m >= 0) {
+      const double kv = kernel_value64<KER>(dot, dist, gamma, coef0, degree);
+      const double qv = i < N ? kv : 0.0;
+      q64[i] = qv;
+      if (i == m) scal[S_KMM] = kv;
+    }
   }
-  norms[i] = (T)nrm;
-  if (m >= 0) {
-    const double kv = kernel_value64<KER>(dot, dist, gamma, coef0, degree);
-    const double qv = i < N ? kv : 0.0;
-    q64[i] = qv;
-    if (i == m) scal[S_KMM] = kv;
+  if (m >= 0) {   // the largest squared norm bounds the kernel values (fixed-point scale)
+    const double mx = block_max(nrm, sh);
+    if (threadIdx.x == 0)
+      atomicMax(reinterpret_cast<unsigned long long*>(scal + S_NMAX),
+                (unsigned long long)__double_as_longlong(mx));
   }
 }
 
@@ -180,11 +208,12 @@ __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64
 template <typename T>
 __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64_t N, int64_t NP,
                                                   double* rhs, double* x, double* xbest, double* r,
-                                                  double* dir, double* bpart, int* flags) {
+                                                  double* dir, double* bpart, int* flags,
+                                                  double* scal) {
   __shared__ double sh[NT / 64];
   const double ym = (double)y[N];
   if (blockIdx.x == 0 && threadIdx.x == 0 && !(ym == 1.0 || ym == -1.0)) flags[F_BADLABEL] = 1;
-  double acc = 0.0;
+  double acc = 0.0, vmax = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     double v = 0.0;
     if (i < N) {
@@ -198,9 +227,14 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
     r[i] = v;
     dir[i] = v;
     acc += v * v;
+    vmax = fmax(vmax, fabs(v));
   }
   const double s = block_sum(acc, sh);
-  if (threadIdx.x == 0) bpart[blockIdx.x] = s;
+  const double mx = block_max(vmax, sh);
+  if (threadIdx.x == 0) {
+    bpart[blockIdx.x] = s;
+    raise_pmax(scal, mx);   // the first product multiplies dir
+  }
 }
 
 __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int64_t nb,
@@ -225,28 +259,28 @@ __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int6
 }
 
 // ------------------------------------------------------------- a5 CG --------
-// q = Q~ d from the tile partials and the rank-one terms (zero beyond N),
-// and the block partials of d^T q (c.p = d).
-__global__ __launch_bounds__(256) void k_cg_gather(const double* __restrict__ part, RankOne c,
-                                                   int64_t NP, int64_t N, double* qv,
-                                                   double* bpart, const double* scal) {
+// q = Q~ d from the product's row sums and the rank-one terms (zero beyond
+// N), and the block partials of d^T q (c.p = d). Block 0 clears the bound on
+// |p| for the next vector.
+__global__ __launch_bounds__(256) void k_cg_gather(RankOne c, int64_t NP, int64_t N, double* qv,
+                                                   double* bpart) {
   __shared__ double sh[NT / 64];
-  __shared__ double rs[NT];
-  if (scal[S_STATUS + ST_DONE] != 0.0) return;
+  if (c.scal[S_STATUS + ST_DONE] != 0.0) return;
   const RankOneSums ro = rank_one_sums(c, sh);
+  const double inv = 1.0 / c.scal[S_FIXSC];
+  const bool bad = c.flags[F_PRODUCT] != 0;
   double prod = 0.0;
-  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
-       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
-    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
-    const int64_t i = r0 + threadIdx.x;
-    if (threadIdx.x < kRowsPerBlock && i < NP) {
-      const double q = i < N ? qtilde_row(c, ro, i, t) : 0.0;
-      qv[i] = q;
-      prod += c.p[i] * q;
-    }
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
+    const double t = product_row(c, i, inv, bad);
+    const double q = i < N ? qtilde_row(c, ro, i, t) : 0.0;
+    qv[i] = q;
+    prod += c.p[i] * q;
   }
   const double t = block_sum(prod, sh);
-  if (threadIdx.x == 0) bpart[blockIdx.x] = t;
+  if (threadIdx.x == 0) {
+    bpart[blockIdx.x] = t;
+    if (blockIdx.x == 0) c.scal[S_PMAX] = 0.0;
+  }
 }
 
 // x += a d and r -= a q (or only x += a d when the residual is about to be
@@ -276,36 +310,38 @@ __global__ __launch_bounds__(256) void k_cg_update(int x_only, const double* __r
   if (broke) return;
   double v = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
-    x[i] += alpha * dir[i];
+    const double xi = x[i] + alpha * dir[i];
+    x[i] = xi;
     if (!x_only) {
       const double ri = r[i] - alpha * qv[i];
       r[i] = ri;
       v += ri * ri;
+    } else {
+      v = fmax(v, fabs(xi));
     }
   }
   if (!x_only) {
     const double t = block_sum(v, sh);
     if (threadIdx.x == 0) bp_out[blockIdx.x] = t;
+  } else {   // the residual recomputation multiplies x next
+    const double mx = block_max(v, sh);
+    if (threadIdx.x == 0) raise_pmax(scal, mx);
   }
 }
 
-// r = rhs - Q~ x from the tile partials (c.p = x), and the block partials
-// of r^T r.
-__global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ part, RankOne c,
-                                                     int64_t NP, int64_t N,
+// r = rhs - Q~ x from the product's row sums (c.p = x), and the block
+// partials of r^T r and of (rhs + r)^T x. Block 0 clears the bound on |p|.
+__global__ __launch_bounds__(256) void k_cg_residual(RankOne c, int64_t NP, int64_t N,
                                                      const double* __restrict__ rhs, double* r,
-                                                     double* bp_out, double* bp_phi,
-                                                     const double* scal) {
+                                                     double* bp_out, double* bp_phi) {
   __shared__ double sh[NT / 64];
-  __shared__ double rs[NT];
-  if (scal[S_STATUS + ST_DONE] != 0.0) return;
+  if (c.scal[S_STATUS + ST_DONE] != 0.0) return;
   const RankOneSums ro = rank_one_sums(c, sh);
+  const double inv = 1.0 / c.scal[S_FIXSC];
+  const bool bad = c.flags[F_PRODUCT] != 0;
   double v = 0.0, e = 0.0;
-  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
-       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
-    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
-    const int64_t i = r0 + threadIdx.x;
-    if (threadIdx.x >= kRowsPerBlock || i >= NP) continue;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
+    const double t = product_row(c, i, inv, bad);
     const double ri = i < N ? rhs[i] - qtilde_row(c, ro, i, t) : 0.0;
     r[i] = ri;
     v += ri * ri;
@@ -316,23 +352,22 @@ __global__ __launch_bounds__(256) void k_cg_residual(const double* __restrict__ 
   if (threadIdx.x == 0) {
     bp_out[blockIdx.x] = t;
     bp_phi[blockIdx.x] = u;
+    if (blockIdx.x == 0) c.scal[S_PMAX] = 0.0;
   }
 }
 
 // ||rhs - Q~ x||^2 partials without touching r (final report only).
-__global__ __launch_bounds__(256) void k_true_residual(const double* __restrict__ part,
-                                                       RankOne c, int64_t NP, int64_t N,
+__global__ __launch_bounds__(256) void k_true_residual(RankOne c, int64_t NP, int64_t N,
                                                        const double* __restrict__ rhs,
                                                        double* bp_out) {
   __shared__ double sh[NT / 64];
-  __shared__ double rs[NT];
   const RankOneSums ro = rank_one_sums(c, sh);
+  const double inv = 1.0 / c.scal[S_FIXSC];
+  const bool bad = c.flags[F_PRODUCT] != 0;
   double v = 0.0;
-  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
-       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
-    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
-    const int64_t i = r0 + threadIdx.x;
-    if (threadIdx.x >= kRowsPerBlock || i >= N) continue;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
+    const double t = product_row(c, i, inv, bad);
+    if (i >= N) continue;
     const double ri = rhs[i] - qtilde_row(c, ro, i, t);
     v += ri * ri;
   }
@@ -385,9 +420,17 @@ __global__ __launch_bounds__(256) void k_cg_direction(const double* __restrict__
         xbest[i] = x[i];
   }
   const double beta = dold != 0.0 ? dnew / dold : 0.0;
-  if (!stall)
-    for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT)
-      dir[i] = r[i] + beta * dir[i];
+  if (!stall) {
+    double dmax = 0.0;
+    for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP;
+         i += (int64_t)gridDim.x * NT) {
+      const double di = r[i] + beta * dir[i];
+      dir[i] = di;
+      dmax = fmax(dmax, fabs(di));
+    }
+    const double mx = block_max(dmax, sh);   // the next product multiplies dir
+    if (threadIdx.x == 0) raise_pmax(scal, mx);
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     scal[S_DHIST + (par ^ 1)] = dnew;
     st[ST_DELTA] = stall ? dbest : dnew;
@@ -415,10 +458,14 @@ __global__ __launch_bounds__(256) void k_warm_start(const double* __restrict__ b
   __shared__ double sh[NT / 64];
   const double dlt = sum_partials(bp_in, nb, sh);
   const double phi = -0.5 * sum_partials(bp_phi, nb, sh);
+  double dmax = 0.0;
   for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
     dir[i] = r[i];
     xbest[i] = x[i];
+    dmax = fmax(dmax, fabs(r[i]));
   }
+  const double mx = block_max(dmax, sh);
+  if (threadIdx.x == 0) raise_pmax(scal, mx);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     double* st = scal + S_STATUS;
     scal[S_DHIST + 0] = dlt;
@@ -473,16 +520,19 @@ __global__ __launch_bounds__(1024) void k_bias(const double* __restrict__ x,
                                                const T* __restrict__ y, double* scal, double invC,
                                                T* __restrict__ alpha_out) {
   __shared__ double sh[1024 / 64];
-  double sx = 0.0, sqx = 0.0;
+  double sx = 0.0, sqx = 0.0, xmax = 0.0;
   for (int64_t i = threadIdx.x; i < N; i += blockDim.x) {
     const double xi = x[i];
     sx += xi;
     sqx += q64[i] * xi;
+    xmax = fmax(xmax, fabs(xi));
     alpha_out[i] = (T)xi;
   }
   sx = block_sum(sx, sh);
   sqx = block_sum(sqx, sh);
+  xmax = block_max(xmax, sh);
   if (threadIdx.x == 0) {
+    scal[S_PMAX] = xmax;   // an optional true-residual product multiplies x next
     alpha_out[N] = (T)(-sx);
     const double qmm = scal[S_KMM] + invC;
     scal[S_B] = (double)y[N] + qmm * sx - sqx;
@@ -597,16 +647,15 @@ __global__ __launch_bounds__(256) void k_pad_vec(const T* __restrict__ src, int6
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_mv_out(const double* __restrict__ part, RankOne c,
-                                                int64_t NP, int64_t N, T* __restrict__ out) {
+__global__ __launch_bounds__(256) void k_mv_out(RankOne c, int64_t NP, int64_t N,
+                                                T* __restrict__ out) {
   __shared__ double sh[NT / 64];
-  __shared__ double rs[NT];
   const RankOneSums ro = rank_one_sums(c, sh);
-  for (int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock; r0 < NP;
-       r0 += (int64_t)gridDim.x * kRowsPerBlock) {
-    const double t = row_slot_sum(part, c.nslots, NP, r0, rs);
-    const int64_t i = r0 + threadIdx.x;
-    if (threadIdx.x < kRowsPerBlock && i < N) out[i] = (T)qtilde_row(c, ro, i, t);
+  const double inv = 1.0 / c.scal[S_FIXSC];
+  const bool bad = c.flags[F_PRODUCT] != 0;
+  for (int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x; i < NP; i += (int64_t)gridDim.x * NT) {
+    const double t = product_row(c, i, inv, bad);
+    if (i < N) out[i] = (T)qtilde_row(c, ro, i, t);
   }
 }
 
@@ -628,9 +677,16 @@ __global__ __launch_bounds__(256) void k_predict_finish(const double* __restrict
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_pad_to_f64(const T* __restrict__ src, int64_t len,
-                                                    double* __restrict__ dst, int64_t len_pad) {
+                                                    double* __restrict__ dst, int64_t len_pad,
+                                                    double* scal) {
+  __shared__ double sh[NT / 64];
   const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  if (i < len_pad) dst[i] = i < len ? (double)src[i] : 0.0;
+  const double v = i < len ? (double)src[i] : 0.0;
+  if (i < len_pad) dst[i] = v;
+  if (scal) {   // a product multiplies dst next
+    const double mx = block_max(fabs(v), sh);
+    if (threadIdx.x == 0) raise_pmax(scal, mx);
+  }
 }
 
 __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t nb, double* scal,
@@ -663,6 +719,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __threadfence();
   constexpr int R = (int)(kFusedMaxNP / NT);
   const RankOneSums ro = rank_one_sums(f.c, sh);
+  const double inv = 1.0 / f.scal[S_FIXSC];
+  const bool bad = f.c.flags[F_PRODUCT] != 0;
   double qr[R], dr[R];
   double g = 0.0;
 #pragma unroll
@@ -670,8 +728,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int64_t i = threadIdx.x + (int64_t)k * NT;
     qr[k] = dr[k] = 0.0;
     if (i < f.NP) {
-      double t = 0.0;
-      for (int64_t sl = 0; sl < f.c.nslots; ++sl) t += a.part[sl * f.NP + i];
+      const double t = product_row(f.c, i, inv, bad);
       const double q = i < f.N ? qtilde_row(f.c, ro, i, t) : 0.0;
       qr[k] = q;
       dr[k] = f.dir[i];
@@ -709,12 +766,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   const double dnew = block_sum(rr, sh);
   const double beta = delta != 0.0 ? dnew / delta : 0.0;
+  double dmax = 0.0;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const int64_t i = threadIdx.x + (int64_t)k * NT;
-    if (i < f.NP) f.dir[i] = rk[k] + beta * dr[k];
+    if (i < f.NP) {
+      const double di = rk[k] + beta * dr[k];
+      f.dir[i] = di;
+      dmax = fmax(dmax, fabs(di));
+    }
   }
+  dmax = block_max(dmax, sh);
   if (threadIdx.x == 0) {
+    f.scal[S_PMAX] = dmax;   // the next launch multiplies dir
     f.scal[S_ALPHA] = alpha;
     f.scal[S_GAMMA] = gam;
     f.scal[S_DHIST + (f.par ^ 1)] = dnew;
@@ -844,9 +908,9 @@ hipError_t launch_tiles_cg(const TileArgs<T>& a0, int kernel, int64_t nwg, const
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x,
                            double* xbest, double* r, double* dir, double* bpart, int* flags,
-                           hipStream_t s) {
+                           double* scal, hipStream_t s) {
   hipLaunchKernelGGL(k_rhs_init<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, y, N, NP, rhs,
-                     x, xbest, r, dir, bpart, flags);
+                     x, xbest, r, dir, bpart, flags, scal);
   return hipGetLastError();
 }
 
@@ -856,10 +920,10 @@ hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, d
   return hipGetLastError();
 }
 
-hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                            double* qv, double* bpart, const double* scal, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
-                     qv, bpart, scal);
+hipError_t launch_cg_gather(const RankOne& c, int64_t NP, int64_t N, double* qv, double* bpart,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_gather, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, c, NP, N, qv,
+                     bpart);
   return hipGetLastError();
 }
 
@@ -871,18 +935,17 @@ hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double*
   return hipGetLastError();
 }
 
-hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, double* bp_phi,
-                              const double* scal, hipStream_t s) {
-  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
-                     rhs, r, bp_out, bp_phi, scal);
+hipError_t launch_cg_residual(const RankOne& c, int64_t NP, int64_t N, const double* rhs, double* r,
+                              double* bp_out, double* bp_phi, hipStream_t s) {
+  hipLaunchKernelGGL(k_cg_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, c, NP, N, rhs,
+                     r, bp_out, bp_phi);
   return hipGetLastError();
 }
 
-hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                                const double* rhs, double* bp_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP,
-                     N, rhs, bp_out);
+hipError_t launch_true_residual(const RankOne& c, int64_t NP, int64_t N, const double* rhs,
+                                double* bp_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_true_residual, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, c, NP, N,
+                     rhs, bp_out);
   return hipGetLastError();
 }
 
@@ -941,10 +1004,8 @@ hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hi
 }
 
 template <typename T>
-hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(k_mv_out<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, part, c, NP, N,
-                     out);
+hipError_t launch_mv_out(const RankOne& c, int64_t NP, int64_t N, T* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_mv_out<T>, dim3((unsigned)cg_blocks(NP)), dim3(NT), 0, s, c, NP, N, out);
   return hipGetLastError();
 }
 
@@ -959,9 +1020,9 @@ hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld,
 
 template <typename T>
 hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len_pad,
-                             hipStream_t s) {
+                             double* scal, hipStream_t s) {
   hipLaunchKernelGGL(k_pad_to_f64<T>, dim3(blocks_for(len_pad)), dim3(NT), 0, s, src, len, dst,
-                     len_pad);
+                     len_pad, scal);
   return hipGetLastError();
 }
 
@@ -1046,16 +1107,16 @@ int64_t linear_predict_part_elems(int64_t n, int64_t d) {
   template hipError_t launch_tiles_cg<T>(const TileArgs<T>&, int, int64_t, const FusedCg&,        \
                                          hipStream_t);                                            \
   template hipError_t launch_rhs_init<T>(const T*, int64_t, int64_t, double*, double*, double*,   \
-                                         double*, double*, double*, int*, hipStream_t);           \
+                                         double*, double*, double*, int*, double*, hipStream_t);  \
   template hipError_t launch_bias<T>(const double*, const double*, int64_t, const T*, double*,    \
                                      double, T*, hipStream_t);                                    \
   template hipError_t launch_single_point<T>(const T*, T*, double*, int*, hipStream_t);           \
   template hipError_t launch_pad_vec<T>(const T*, int64_t, T*, int64_t, hipStream_t);             \
-  template hipError_t launch_mv_out<T>(const double*, const RankOne&, int64_t, int64_t, T*,       \
-                                       hipStream_t);                                              \
+  template hipError_t launch_mv_out<T>(const RankOne&, int64_t, int64_t, T*, hipStream_t);       \
   template hipError_t launch_predict_finish<T>(const double*, int64_t, int64_t, int64_t, double,  \
                                                T*, int32_t*, const int*, hipStream_t);            \
-  template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, hipStream_t);   \
+  template hipError_t launch_pad_to_f64<T>(const T*, int64_t, double*, int64_t, double*,          \
+                                           hipStream_t);                                          \
   template hipError_t launch_linear_predict<T>(const T*, const T*, int64_t, int64_t, const T*,    \
                                                int64_t, double, double*, double*, double*, T*,    \
                                                int32_t*, int*, hipStream_t);

@@ -37,6 +37,14 @@ enum Scalar : int {
   S_BEST = 16,   // smallest true r^T r so far (start, residual recomputations),
                  // double-buffered by recomputation: [16], [17]
   S_PHI = 18,    // smallest CG energy -(rhs + r)^T x / 2 so far, likewise: [18], [19]
+  // Fixed-point row sums of the symmetric products (tiles.h): [20] max |p_j| of
+  // the vector the next product multiplies (raised with an integer atomic max
+  // on its bits by the kernel that writes the vector, cleared by the kernel
+  // that reads the product), [21] max ||x_i||^2, [22] the scale 2^s the last
+  // product used
+  S_PMAX = 20,
+  S_NMAX = 21,
+  S_FIXSC = 22,
   S_COUNT = 24
 };
 enum StatusField : int { ST_DELTA = 0, ST_CURV = 1, ST_STEP = 2, ST_ITER = 3, ST_DONE = 4,
@@ -51,31 +59,31 @@ inline int64_t vec_blocks(int64_t len) {
   return b < kVecBlocks ? (b > 0 ? b : 1) : kVecBlocks;
 }
 
-// The training's CG vector kernels run one block per 32 rows of the padded
-// vectors (the gather sums each row's tile partial slots with 8 thread
-// groups, so many loads are in flight even for short vectors), at most
-// kVecBlocks, striding beyond that.
-constexpr int64_t kSlotGroups = 8, kRowsPerBlock = 256 / kSlotGroups;
-inline int64_t cg_blocks(int64_t NP) {
-  const int64_t b = NP / kRowsPerBlock;
-  return b < kVecBlocks ? (b > 0 ? b : 1) : kVecBlocks;
-}
+// The training's CG vector kernels (the readers of a product included: each
+// row's sum is two words) run one block per 256 rows of the padded vectors,
+// at most kVecBlocks, striding beyond that.
+inline int64_t cg_blocks(int64_t NP) { return vec_blocks(NP); }
 
 // Flags raised by kernels (int32 each).
-enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_COUNT = 4 };
+// F_PRODUCT: a symmetric product had a row sum that is not finite (its
+// entries then come out as NaN, so CG reports a breakdown).
+enum Flag : int { F_NONFINITE = 0, F_BADLABEL = 1, F_PRODUCT = 2, F_COUNT = 4 };
 
 
-// The rank-one and diagonal terms of Q~ p that the symmetric tiles leave out
-// (Eq. (13)): (Q~ p)_i = (K p)_i + (Q_mm - q_i) S - T + p_i / C for i < N,
-// with S = sum_j p_j, T = sum_j q_j p_j (summed from the diagonal tiles'
-// per-panel partials in a fixed order) and Q_mm = k(x_m, x_m) + 1/C.
+// One symmetric product as its readers see it: (K p)_i in the fixed-point
+// accumulators of the tiles, and the rank-one and diagonal terms of Q~ p that
+// the tiles leave out (Eq. (13)): (Q~ p)_i = (K p)_i + (Q_mm - q_i) S - T +
+// p_i / C for i < N, with S = sum_j p_j, T = sum_j q_j p_j (summed from the
+// diagonal tiles' per-panel partials in a fixed order) and
+// Q_mm = k(x_m, x_m) + 1/C. A reader clears the accumulators it reads.
 struct RankOne {
   const double* pq;    // 2 nT panel partials: S_I, then T_I
   int64_t nT;
-  int64_t nslots;      // tile partial slots to sum per row
+  int64_t* acc;        // fixed-point row sums (two words per row)
   const double* q64;   // q_i, zero beyond N
   const double* p;     // the vector multiplied, zero beyond N
-  const double* scal;  // k(x_m, x_m) at S_KMM
+  double* scal;        // k(x_m, x_m) at S_KMM, the product's scale at S_FIXSC
+  const int* flags;    // F_PRODUCT
   double invC;
 };
 
@@ -89,10 +97,9 @@ struct FusedCg {
   int64_t NP, N, iter, hist_cap;
   int par;            // r^T r of the current iterate lives in S_DHIST + par
 };
-// Largest padded length and partial-slot count the fused iteration handles:
-// one workgroup reads every partial (NP x nslots doubles) and keeps each
-// thread's rows (NP / 256) in registers.
-constexpr int64_t kFusedMaxNP = 1024, kFusedMaxParts = 1 << 16;
+// Largest padded length the fused iteration handles: one workgroup reads every
+// row sum and keeps each thread's rows (NP / 256) in registers.
+constexpr int64_t kFusedMaxNP = 1024;
 
 // The symmetric tiles' visit order (GROUP x GROUP super-tiles), packed
 // (I << 16) | J, nT (nT + 1) / 2 entries.
@@ -113,7 +120,7 @@ hipError_t launch_tiles_sym(const TileArgs<T>& a, int kernel, int part, int64_t 
 template <typename T>
 hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipStream_t s);
 // A whole CG iteration in one launch for small problems (NP <= kFusedMaxNP,
-// NP x partial slots <= kFusedMaxParts, a single whole-tile launch per
+// a single whole-tile launch per
 // product): the symmetric tiles of q = Q~ d, then the workgroup that
 // finishes last (an atomic ticket after a device-scope release fence) adds the
 // rank-one terms and does the update and the new direction, with the same
@@ -122,25 +129,26 @@ hipError_t launch_tiles_gen(const TileArgs<T>& a, int kernel, int64_t nTr, hipSt
 template <typename T>
 hipError_t launch_tiles_cg(const TileArgs<T>& a, int kernel, int64_t nwg, const FusedCg& f,
                            hipStream_t s);
+// rhs = ybar - y_m 1, x = xbest = 0, r = dir = rhs, the block partials of
+// r^T r; raises scal[S_PMAX] to max |dir| (the first product multiplies it).
 template <typename T>
 hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, double* x,
                            double* xbest, double* r, double* dir, double* bpart, int* flags,
-                           hipStream_t s);
+                           double* scal, hipStream_t s);
 // CG kernels: once the status says done, every later kernel of the queue
 // returns at once, so the host may enqueue iterations ahead of the test.
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
                                 hipStream_t s);
 // q = Q~ dir (c.p = dir) and the block partials of dir^T q.
-hipError_t launch_cg_gather(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                            double* qv, double* bpart, const double* scal, hipStream_t s);
+hipError_t launch_cg_gather(const RankOne& c, int64_t NP, int64_t N, double* qv, double* bpart,
+                            hipStream_t s);
 hipError_t launch_cg_update(int x_only, const double* bp_in, int64_t nb, double* scal, int par,
                             const double* dir, const double* qv, double* x, double* r,
                             double* bp_out, int64_t NP, hipStream_t s);
 // r = rhs - Q~ x (c.p = x), the block partials of r^T r and those of
 // (rhs + r)^T x (minus twice the CG energy of x).
-hipError_t launch_cg_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                              const double* rhs, double* r, double* bp_out, double* bp_phi,
-                              const double* scal, hipStream_t s);
+hipError_t launch_cg_residual(const RankOne& c, int64_t NP, int64_t N, const double* rhs, double* r,
+                              double* bp_out, double* bp_phi, hipStream_t s);
 // Warm start: delta = r0^T r0 from the block partials, dir = r0, the start as
 // the best iterate so far (its residual and energy), done if already below
 // the stop threshold.
@@ -172,21 +180,21 @@ hipError_t launch_single_point(const T* y, T* alpha_out, double* scal, int* flag
 template <typename T>
 hipError_t launch_pad_vec(const T* src, int64_t len, T* dst, int64_t len_pad, hipStream_t s);
 template <typename T>
-hipError_t launch_mv_out(const double* part, const RankOne& c, int64_t NP, int64_t N, T* out,
-                         hipStream_t s);
+hipError_t launch_mv_out(const RankOne& c, int64_t NP, int64_t N, T* out, hipStream_t s);
 // scores = b + the sum of nslots partial slots; nothing is written if the
 // input flags report a non-finite point.
 template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
                                  double b, T* scores, int32_t* labels, const int* flags,
                                  hipStream_t s);
+// dst = src zero-padded, in fp64; with scal, also raises scal[S_PMAX] to max |dst|.
 template <typename T>
 hipError_t launch_pad_to_f64(const T* src, int64_t len, double* dst, int64_t len_pad,
-                             hipStream_t s);
+                             double* scal, hipStream_t s);
 hipError_t launch_finish_sum(const double* bpart, int64_t nb, double* scal, int slot,
                              hipStream_t s);
-hipError_t launch_true_residual(const double* part, const RankOne& c, int64_t NP, int64_t N,
-                                const double* rhs, double* bp_out, hipStream_t s);
+hipError_t launch_true_residual(const RankOne& c, int64_t NP, int64_t N, const double* rhs,
+                                double* bp_out, hipStream_t s);
 
 // Linear-kernel decision values through w = sum_i alpha_i x_i (Eq. (15)).
 // part: linear_predict_part_elems(n, d) doubles; w: d doubles; f: n_test

@@ -47,14 +47,21 @@ struct TileArgs {
   int degree;
   int64_t nTc;   // column tiles (general mode); tiles per side (symmetric mode)
   int64_t ksplit;  // symmetric mode: workgroups per tile, each over nkb / ksplit feature
-                   // blocks (an even count). Linear kernel, whole tiles: row partials
-                   // of tile (I, J) and split s go to slot J ksplit + s, column
-                   // partials to I ksplit + s. Split launches park inner products in
+                   // blocks (an even count). Linear kernel, whole tiles: every split
+                   // adds its share of the row and column sums (the kernel value is
+                   // the inner product itself). Split launches park inner products in
                    // gpart instead and a fixup launch finishes each tile.
   int64_t tile_offset;  // symmetric mode: first tile of the launch in the visit order
   T* gpart;             // split launches: parked inner products, ksplit 128^2 per tile
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
-  double* part;  // partial sums, part[slot * part_ld + row]
+  double* part;  // general mode: partial sums, part[slot * part_ld + row]
+  // symmetric mode: each row's sum over tiles, in fixed point (see fixed_add):
+  // acc[2 row] the low 32-bit limbs, acc[2 row + 1] the signed high limbs
+  int64_t* acc;
+  // symmetric mode: fx[0] = max |p_j|, fx[1] = max ||x_i||^2 (the bounds of the
+  // fixed-point scale); fx[2] receives the scale 2^s the launch used
+  double* fx;
+  int* fx_bad;          // symmetric mode: raised when a row sum is not finite
   const double* stop;   // symmetric mode: nonzero once CG has stopped (the launch then
                         // returns at once), or null
   int64_t part_ld;

@@ -171,6 +171,49 @@ __device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
   I = t - j * (j + 1) / 2;
 }
 
+// ------------------------------------------------ fixed-point row sums ----
+// The symmetric tiles add their row and column sums into one accumulator per
+// row with integer atomics, which makes the total independent of the order
+// the tiles finish in (fp64 atomics would not be) and keeps the memory at two
+// 64-bit words per row. A product's scale 2^s is fixed before it starts from
+// bounds on |k(x_i, x_j)| and |p_j|: one tile's sum for a row is below
+// 128 kmax pmax, so with s = 61 - e, 2^e > 256 kmax pmax, every scaled sum
+// |v 2^s| < 2^60. It is rounded to an integer X once (a spacing 2^-s of about
+// 2^-54 kmax pmax, far finer than the fp64 rounding of the sum itself) and
+// added as two limbs, X mod 2^32 (unsigned) and floor(X / 2^32) (signed), so
+// neither 64-bit word can overflow for any number of tiles below 2^31. The
+// kernel that reads a row (fixed_take) restores X's sum exactly and rounds it
+// once to fp64.
+template <int KER, typename T>
+__device__ inline double fixed_scale(const TileArgs<T>& a) {
+  const double pmax = a.fx[0], nmax = a.fx[1];
+  double km = 1.0;   // bound on |k(x_i, x_j)|: RBF values are at most 1
+  if constexpr (KER == KLIN) {
+    km = nmax;       // |<x, z>| <= ||x|| ||z||
+  } else if constexpr (KER == KPOLY) {
+    const double base = fabs((double)a.gamma) * nmax + fabs((double)a.coef0);
+    for (int e = 0; e < a.degree; ++e) km *= base;
+  }
+  const double bound = 256.0 * km * pmax;
+  if (!(bound > 0.0) || !(bound < 1e300)) return 1.0;   // p = 0 (sums 0) or no usable bound
+  int e = 0;
+  (void)frexp(bound, &e);   // bound < 2^e
+  return ldexp(1.0, 61 - e);
+}
+
+__device__ inline void fixed_add(int64_t* acc, int* bad, int64_t row, double v, double scale) {
+  const double t = v * scale;
+  if (!(fabs(t) < 0x1p62)) {   // not finite, or beyond the bound: the product is unusable
+    *bad = 1;
+    return;
+  }
+  const int64_t X = __double2ll_rn(t);
+  const unsigned long long lo = (unsigned long long)X & 0xffffffffull;
+  const unsigned long long hi = (unsigned long long)(X >> 32);   // two's complement bits
+  atomicAdd(reinterpret_cast<unsigned long long*>(acc + 2 * row), lo);
+  atomicAdd(reinterpret_cast<unsigned long long*>(acc + 2 * row + 1), hi);
+}
+
 // Tile rows per band of the general-mode visit order.
 constexpr int64_t kBandRows = 8;
 
@@ -188,14 +231,15 @@ __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // matrix cores. The epilogue turns G into kernel values and folds them into
 // row sums (times p_j) and, off the diagonal, column sums (times p_i), so
 // that each off-diagonal tile serves both triangles. Row and column sums are
-// reduced across lanes and waves in a fixed order and written as fp64
-// partials, one slot per tile column (rows of block I) or tile row (rows of
-// block J).
+// reduced across lanes and waves in a fixed order and added, in fixed point,
+// to the rows' accumulators (symmetric mode: fixed_add), or written as fp64
+// partials, one slot per tile column (general mode).
 //
-// PART splits a symmetric tile's features over a.ksplit workgroups without
-// separate partial slots: kPartial workgroups park their raw inner products
-// G (the accumulators) in a.gpart and stop; a kFixup launch, one workgroup
-// per tile, sums the parked splits in split order and runs the epilogue.
+// PART splits a symmetric tile's features over a.ksplit workgroups for the
+// kernels whose value needs the whole inner product: kPartial workgroups park
+// their raw inner products G (the accumulators) in a.gpart and stop; a kFixup
+// launch, one workgroup per tile, sums the parked splits in split order and
+// runs the epilogue.
 //
 // The body returns false when the launch found CG already stopped (nothing
 // done), true otherwise.
@@ -258,7 +302,6 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // takes split v % KS of tile v / KS of this launch, which starts at
   // a.tile_offset of the visit order.
   const int64_t KS = (SYM && (KER == KLIN || PART != kWhole)) ? a.ksplit : 1;
-  const int64_t SS = PART == kWhole ? KS : 1;   // partial slots per tile row / column
   int64_t ks = 0, trel = 0;
   const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's slot
   if constexpr (SYM) {
@@ -497,6 +540,11 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // their products with the vector and all sums in fp64, so an fp32 product
   // uses the fp64 CG direction as it is instead of a rounded copy.
   const bool diag = SYM && (I == J);
+  double fxs = 1.0;   // fixed-point scale of the row sums (symmetric mode)
+  if constexpr (SYM) {
+    fxs = fixed_scale<KER>(a);
+    if (blockIdx.x == 0 && tid == 0) a.fx[2] = fxs;   // every workgroup finds the same
+  }
   T nBj[CB];
   double pBj[CB];
 #pragma unroll
@@ -599,13 +647,14 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_N; ++w) s += red_r[w][tid];
-    a.part[(J * SS + ks) * a.part_ld + I * BM + tid] = s;
+    if constexpr (SYM) fixed_add(a.acc, a.fx_bad, I * BM + tid, s, fxs);
+    else a.part[J * a.part_ld + I * BM + tid] = s;
   } else if (SYM && !diag && tid < 2 * BM) {
     const int c = tid - BM;
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < WAVES_M; ++w) s += red_c[w][c];
-    a.part[(I * SS + ks) * a.part_ld + J * BM + c] = s;
+    fixed_add(a.acc, a.fx_bad, J * BM + c, s, fxs);
   }
   if constexpr (SYM) {
     // A diagonal tile also leaves its panel's share of the rank-one terms:

@@ -50,6 +50,22 @@ def test_workspace_sizes():
     assert L.lssvm_tile_size(5) == 0
 
 
+def test_workspace_grows_with_the_points_not_their_square():
+    """A product's row sums take two 64-bit words per row (fixed-point
+    accumulators), not a partial slot per tile column: at 2^20 points of 16
+    features the training workspace is the points' own layout (2^20 x 64 x 4
+    bytes, features padded to two blocks) plus about a fifth of a GiB (the
+    tile visit order, n^2 / 8192 bytes, is the only quadratic term). A slot
+    per tile column would have been n^2 / 16 bytes = 64 GiB."""
+    L = P.lib()
+    n = 1 << 20
+    ws = L.lssvm_workspace_bytes(n, 16, 1)
+    layout = n * 64 * 4
+    assert ws < 4 << 30
+    assert ws - layout < (n * n // 16) // 200
+    assert L.lssvm_workspace_bytes(2 * n, 16, 1) < 3 * ws
+
+
 def test_tile_split():
     """The linear kernel's feature split: 1 for the other kernels and for large
     problems, a power of two up to 16 for small ones, always leaving an even

@@ -231,8 +231,8 @@ def test_matvec_rejects_nonfinite(torch_dev):
 @pytest.mark.parametrize("dtype,kernel,n,d", [("f32", "rbf", 1 << 20, 16),
                                               ("f64", "linear", (1 << 19) + 77, 24)])
 def test_matvec_large_n_sampled_rows(torch_dev, dtype, kernel, n, d):
-    """The implicit product at n up to 2^20 points (33.6M tiles, a 69 GB
-    workspace of tile partials): sampled rows, including the last row and
+    """The implicit product at n up to 2^20 points (33.6M tiles adding into
+    2^21 fixed-point words): sampled rows, including the last row and
     the ragged last tile, against the oracle's rows computed one by one; over
     all rows, p^T Q~ p > 0 (Q~ is SPD) and every entry finite."""
     torch, dev = torch_dev
