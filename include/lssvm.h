@@ -271,13 +271,22 @@ const char* lssvm_last_error(void);
  * 0 for an unknown dtype. Informational: sizes need no padding by the caller. */
 int32_t lssvm_tile_size(int32_t dtype);
 
-/* Workgroups per upper-triangle tile in the implicit products of lssvm_train
- * and lssvm_matvec for n >= 2 points of d features: 1, except for the linear
- * kernel on problems with few tiles, whose features are split over 2..16
- * workgroups per tile (the partial sums add up because the linear kernel
- * value is the inner product itself) so that the tiles fill the device.
- * 0 for arguments out of range. Informational. */
-int32_t lssvm_tile_split(int64_t n, int64_t d, int32_t dtype, int32_t kernel);
+/* How the implicit products of lssvm_train and lssvm_matvec lay out their
+ * upper-triangle tiles over workgroups for n >= 2 points of d features.
+ * On success writes plan[0..2] (host memory, caller-owned):
+ *   plan[0]  workgroups per tile in the full rounds: 1, except for the
+ *            linear kernel on problems with few tiles, whose features are
+ *            split over 2..16 workgroups per tile (the partial sums add up
+ *            because the linear kernel value is the inner product itself);
+ *   plan[1]  tiles of a last partial round that run split finer (0 if none):
+ *            the linear kernel runs them in a second launch, split the same
+ *            additive way; the other kernels park their partial inner
+ *            products and sum them in a fix-up launch;
+ *   plan[2]  workgroups per such tile (plan[0] when plan[1] is 0).
+ * Every split leaves an even number of feature blocks per workgroup.
+ * Returns LSSVM_EINVAL (plan untouched) for n, d, dtype or kernel out of
+ * range or a null plan. Informational. */
+int lssvm_tile_plan(int64_t n, int64_t d, int32_t dtype, int32_t kernel, int64_t* plan);
 
 #ifdef __cplusplus
 }

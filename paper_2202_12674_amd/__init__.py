@@ -7,10 +7,11 @@ include/lssvm.h; PyTorch supplies device memory and streams only.
 """
 from ._binding import (F32, F64, LINEAR, POLY, RBF, LssvmError, TrainResult,  # noqa: F401
                        alloc_workspace, cg_step, cg_step_noalloc, host_contexts, last_error, lib,
-                       matvec, mfma_peak, predict, predict_workspace_bytes, train,
+                       matvec, mfma_peak, predict, predict_workspace_bytes, tile_plan, train,
                        workspace_bytes)
 from .build import LIB_PATH  # noqa: F401
 
 __all__ = ["train", "predict", "matvec", "cg_step", "cg_step_noalloc", "mfma_peak",
            "workspace_bytes", "predict_workspace_bytes", "alloc_workspace", "host_contexts",
+           "tile_plan",
            "LssvmError", "TrainResult", "lib", "last_error"]

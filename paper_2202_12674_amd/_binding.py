@@ -106,8 +106,8 @@ _SIGS = {
                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                         ctypes.c_int64, ctypes.c_int32]),
     "lssvm_tile_size": (ctypes.c_int32, [ctypes.c_int32]),
-    "lssvm_tile_split": (ctypes.c_int32, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
-                                          ctypes.c_int32]),
+    "lssvm_tile_plan": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.POINTER(ctypes.c_int64)]),
 }
 
 
@@ -396,6 +396,16 @@ def cg_step_noalloc(x, r, d, q, scalars):
         _check(lib().lssvm_cg_step_noalloc(N, _dev_ptr(x, "x"), _dev_ptr(r, "r"),
                                            _dev_ptr(d, "d"), _dev_ptr(q, "q"),
                                            _dev_ptr(scalars, "scalars"), _stream(x.device)))
+
+
+def tile_plan(n: int, d: int, dtype: str, kernel: str) -> tuple:
+    """lssvm_tile_plan: (workgroups per tile, tiles of the finer-split last
+    round, workgroups per such tile) of the implicit product for n points of
+    d features; dtype "f64" or "f32", kernel "linear", "poly" or "rbf"."""
+    plan = (ctypes.c_int64 * 3)()
+    _check(lib().lssvm_tile_plan(int(n), int(d), {"f64": 0, "f32": 1}[dtype],
+                                 {"linear": 0, "poly": 1, "rbf": 2}[kernel], plan))
+    return tuple(int(v) for v in plan)
 
 
 def host_contexts() -> int:

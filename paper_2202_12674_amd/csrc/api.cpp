@@ -83,6 +83,8 @@ struct Geometry {
   int64_t NP;       // nT * tile: padded length of every CG vector
   int64_t nb;       // blocks of the CG vector kernels over NP (block partials per reduction)
   int64_t ksplit;   // linear kernel: workgroups per tile, each over a share of the features
+  int64_t lin_tail_q;      // linear kernel: tiles of the last partial round (or 0), in a
+  int64_t lin_tail_split;  // second launch split this many ways
   int64_t tail_q;   // other kernels: tiles of the last partial round that are split (or 0)
   int64_t tail_split;  // ... over this many workgroups each
 };
@@ -94,9 +96,9 @@ struct Geometry {
 // as one launch: the product's tiles and, in the last workgroup, the vector
 // work (launch_tiles_cg). Their iterations are launch-bound: four dependent
 // launches of a few microseconds each against a product of ~10 us.
-inline bool fused_iteration(const Geometry& g, int64_t ksplit) {
-  return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP &&
-         (ksplit > 1 || g.tail_q == 0);   // one whole-tile launch per product
+inline bool fused_iteration(const Geometry& g, int32_t kernel) {
+  const bool one_launch = kernel == LSSVM_LINEAR ? g.lin_tail_q == 0 : g.tail_q == 0;
+  return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP && one_launch;
 }
 
 inline int64_t tri_count(int64_t nT) { return nT * (nT + 1) / 2; }
@@ -107,28 +109,64 @@ constexpr int64_t kResidentTiles = 512;
 #define LSSVM_LINEAR_SPLIT_MAX 16
 #endif
 
+#ifndef LSSVM_LINEAR_TAIL
+#define LSSVM_LINEAR_TAIL 1
+#endif
+
+// Finer split of the linear kernel's tiles in a last partial round that
+// already runs S ways: the largest T (up to 64) with Q T within one round of
+// resident workgroups and an even number of feature blocks per share.
+inline int64_t linear_tail_split(int64_t Q, int64_t S, int64_t nkb) {
+  int64_t T = S;
+  while (LSSVM_LINEAR_TAIL && T < 64 && Q * T * 2 <= kResidentTiles && nkb % (4 * T) == 0)
+    T *= 2;
+  return T;
+}
+
 // Feature split of the linear kernel's tiles. A product of W tiles split S
-// ways runs in ceil(W S / R) rounds of R resident workgroups, each round as
-// long as 1/S of a tile plus a fixed cost of about two feature blocks (the
-// first block's load latency and the epilogue). Small problems, whose tiles
-// fill the chip once and leave a sliver for a second round, gain most; large
-// ones keep S = 1. S halves the block count, which must stay even.
-inline int64_t linear_split(int64_t nT, int64_t nkb) {
+// ways runs in rounds of R resident workgroups, each as long as 1/S of a
+// tile plus a fixed cost of about two feature blocks (the first block's load
+// latency and the epilogue). The full rounds take floor(W S / R) of those;
+// the Q tiles left for a last partial round run in a launch of their own,
+// split T >= S ways (the feature shares add into the row sums like any
+// split's, so no fixup is needed), which takes 1/T of a tile plus the fixed
+// cost. S (and T) halve the block count, which must stay even. A problem of
+// one round or less keeps its tiles in one launch.
+inline void linear_plan(int64_t nT, int64_t nkb, int64_t* split, int64_t* q, int64_t* tail_split) {
   const int64_t W = tri_count(nT);
   const double f = 2.0 / (double)nkb;
-  auto cost = [&](int64_t S) {
-    return (double)((W * S + kResidentTiles - 1) / kResidentTiles) * (1.0 / (double)S + f);
+  auto plan = [&](int64_t S, int64_t* Q, int64_t* T) {
+    *Q = 0;
+    *T = S;
+    if (W * S <= kResidentTiles) return 1.0 / (double)S + f;
+    const int64_t full = W * S / kResidentTiles;
+    const int64_t left = W - full * (kResidentTiles / S);
+    double c = (double)full * (1.0 / (double)S + f);
+    if (left > 0) {
+      const int64_t t = linear_tail_split(left, S, nkb);
+      c += 1.0 / (double)t + f;
+      if (t > S) {
+        *Q = left;
+        *T = t;
+      }
+    }
+    return c;
   };
-  int64_t best = 1;
-  double best_cost = cost(1);
+  int64_t best = 1, bq, bt;
+  double best_cost = plan(1, &bq, &bt);
   for (int64_t S = 2; S <= LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0; S *= 2) {
-    const double c = cost(S);
+    int64_t Q, T;
+    const double c = plan(S, &Q, &T);
     if (c < 0.95 * best_cost) {   // a clear gain only: each split adds workgroups and atomics
       best = S;
       best_cost = c;
+      bq = Q;
+      bt = T;
     }
   }
-  return best;
+  *split = best;
+  *q = bq;
+  *tail_split = bt;
 }
 
 // The tiles beyond the last full round of resident workgroups run one per
@@ -157,7 +195,7 @@ Geometry geometry(int64_t n, int64_t d) {
   g.nT = (g.N + g.tile - 1) / g.tile;
   g.NP = g.nT * g.tile;
   g.nb = cg_blocks(g.NP);
-  g.ksplit = linear_split(g.nT, g.d_pad / g.bk);
+  linear_plan(g.nT, g.d_pad / g.bk, &g.ksplit, &g.lin_tail_q, &g.lin_tail_split);
   tail_plan(g.nT, g.d_pad / g.bk, &g.tail_q, &g.tail_split);
   return g;
 }
@@ -489,8 +527,15 @@ template <typename T>
 hipError_t launch_product(const Geometry& g, TileArgs<T> a, int32_t kernel, T* gpart,
                           hipStream_t s) {
   const int64_t W = tri_count(g.nT);
-  if (a.ksplit > 1 || g.tail_q == 0)
-    return launch_tiles_sym<T>(a, kernel, kWhole, W * a.ksplit, s);
+  if (kernel == LSSVM_LINEAR) {   // feature splits add up: the tail only splits finer
+    const int64_t F = W - g.lin_tail_q;
+    hipError_t e = launch_tiles_sym<T>(a, kernel, kWhole, F * a.ksplit, s);
+    if (e != hipSuccess || g.lin_tail_q == 0) return e;
+    a.tile_offset = F;
+    a.ksplit = g.lin_tail_split;
+    return launch_tiles_sym<T>(a, kernel, kWhole, g.lin_tail_q * g.lin_tail_split, s);
+  }
+  if (g.tail_q == 0) return launch_tiles_sym<T>(a, kernel, kWhole, W, s);
   const int64_t F = W - g.tail_q;
   hipError_t e = launch_tiles_sym<T>(a, kernel, kWhole, F, s);
   if (e != hipSuccess) return e;
@@ -621,7 +666,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   // threshold (with a quarter to spare).
   int64_t it_prev = 0, need = max_iter;
   double delta_prev = delta;
-  const bool fused = fused_iteration(g, tile_split(g, kernel));
+  const bool fused = fused_iteration(g, kernel);
   if (fused && !done) LSSVM_HIP(hipMemsetAsync(w.ticket, 0, sizeof(unsigned), s));
   // A fused iteration takes ~15 us and a status read-back ~30 us: small
   // problems start with 8 iterations queued (those run past the stop return at
@@ -957,12 +1002,21 @@ int32_t lssvm_tile_size(int32_t dtype) {
   return 0;
 }
 
-int32_t lssvm_tile_split(int64_t n, int64_t d, int32_t dtype, int32_t kernel) {
-  if (n < 2 || d < 1 || n > (int64_t(1) << 22) || d > (int64_t(1) << 21)) return 0;
-  if (kernel != LSSVM_LINEAR && kernel != LSSVM_POLY && kernel != LSSVM_RBF) return 0;
-  if (dtype == LSSVM_F64) return (int32_t)tile_split(geometry<double>(n, d), kernel);
-  if (dtype == LSSVM_F32) return (int32_t)tile_split(geometry<float>(n, d), kernel);
-  return 0;
+int lssvm_tile_plan(int64_t n, int64_t d, int32_t dtype, int32_t kernel, int64_t* plan) {
+  clear_error();
+  if (n < 2 || d < 1 || n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
+    return fail(LSSVM_EINVAL, "tile_plan: need 2 <= n <= 2^22 and 1 <= d <= 2^21");
+  if (kernel != LSSVM_LINEAR && kernel != LSSVM_POLY && kernel != LSSVM_RBF)
+    return fail(LSSVM_EINVAL, "tile_plan: unknown kernel");
+  if (dtype != LSSVM_F64 && dtype != LSSVM_F32) return fail(LSSVM_EINVAL, "tile_plan: unknown dtype");
+  if (!plan) return fail(LSSVM_EINVAL, "tile_plan: null plan");
+  const Geometry g = dtype == LSSVM_F64 ? geometry<double>(n, d) : geometry<float>(n, d);
+  const bool lin = kernel == LSSVM_LINEAR;
+  plan[0] = tile_split(g, kernel);
+  plan[1] = lin ? g.lin_tail_q : g.tail_q;
+  plan[2] = lin ? g.lin_tail_split : g.tail_split;
+  if (plan[1] == 0) plan[2] = plan[0];
+  return LSSVM_OK;
 }
 
 const char* lssvm_last_error(void) { return g_last_error.c_str(); }

@@ -21,7 +21,7 @@ TOL_ALPHA = BAR_SOL
 
 __all__ = ["GOLDEN", "TOL_MV", "TOL_ALPHA", "BAR_MV", "BAR_SOL", "rel_err", "log", "spec_of",
            "kw_of", "small_cfg", "data_of", "to_dev", "golden", "golden_tight", "SPLIT_SHAPES",
-           "tail_plan", "TAIL_SHAPES", "random_cases", "random_large_cases",
+           "TAIL_SHAPES", "random_cases", "random_large_cases",
            "fp32_sensitivity", "OracleRef", "oracle_ref", "check_train", "labels_match"]
 
 
@@ -72,32 +72,21 @@ def golden(name):
 
 # Linear products of few tiles split each tile's features over several
 # workgroups; these shapes give every split the library uses.
-SPLIT_SHAPES = [("f64", 4096, 256, 2), ("f64", 4096, 1024, 4), ("f64", 1000, 256, 8),
-                ("f64", 600, 1024, 16), ("f32", 2000, 1024, 2), ("f32", 1000, 256, 4),
-                ("f32", 1000, 1024, 8), ("f32", 600, 1024, 16)]
+# (dtype, n, d, plan) of the linear kernel's feature splits; plan is the
+# library's (workgroups per tile, tiles of the finer-split last round,
+# workgroups per such tile): splits without a tail, a tail over the split
+# full rounds, and a tail after unsplit ones (the 4096 x 1024 fp64 workload).
+SPLIT_SHAPES = [("f64", 600, 256, (8, 0, 8)), ("f64", 2000, 512, (4, 8, 16)),
+                ("f64", 1000, 2048, (16, 4, 64)), ("f64", 3000, 256, (2, 44, 8)),
+                ("f64", 4096, 1024, (1, 16, 32)), ("f32", 1000, 256, (4, 0, 4)),
+                ("f32", 600, 1024, (16, 0, 16)), ("f32", 2000, 1024, (4, 8, 16)),
+                ("f32", 3000, 512, (2, 44, 8)), ("f32", 4096, 256, (1, 16, 4))]
 
-
-def tail_plan(n, d, dtype):
-    """(tail tiles, splits) of a symmetric product as the library plans it: the
-    tiles after the last full round of 512 workgroups, split 4..16 ways when
-    they are at most a quarter round."""
-    bk = 16 if dtype == "f64" else 32
-    nkb = -(-d // (2 * bk)) * 2
-    nT = -(-(n - 1) // 128)
-    Q = nT * (nT + 1) // 2 % 512
-    S = 1
-    while S < 16 and Q * S * 2 <= 512 and nkb % (4 * S) == 0:
-        S *= 2
-    return (Q, S) if Q > 0 and S >= 4 else (0, 1)
-
-
-# Tiles beyond the last full round are split over several workgroups whose
-# inner products a fixup launch sums: every tile in the tail (600 points), one
-# full round plus 16 tail tiles (4096 points), a linear product without the
-# feature split (12288 points).
-TAIL_SHAPES = [("f64", "rbf", 600, 256, (15, 8)), ("f32", "poly", 600, 256, (15, 4)),
-               ("f64", "poly", 4096, 256, (16, 8)), ("f32", "rbf", 4096, 512, (16, 8)),
-               ("f64", "linear", 12288, 1024, (48, 8))]
+# (dtype, kernel, n, d, plan): the tiles after the last full round of 512
+# workgroups split 4..16 ways, parked and fixed up (linear: added up).
+TAIL_SHAPES = [("f64", "rbf", 600, 256, (1, 15, 8)), ("f32", "poly", 600, 256, (1, 15, 4)),
+               ("f64", "poly", 4096, 256, (1, 16, 8)), ("f32", "rbf", 4096, 512, (1, 16, 8)),
+               ("f64", "linear", 12288, 1024, (1, 48, 8))]
 
 
 def random_cases(count=24, seed=2026):

@@ -66,27 +66,50 @@ def test_workspace_grows_with_the_points_not_their_square():
     assert L.lssvm_workspace_bytes(2 * n, 16, 1) < 3 * ws
 
 
-def test_tile_split():
-    """The linear kernel's feature split: 1 for the other kernels and for large
-    problems, a power of two up to 16 for small ones, always leaving an even
-    number of feature blocks per workgroup; 0 outside the supported range."""
+def test_tile_plan():
+    """The launch plan of the implicit product: pinned for the five benchmark
+    workloads and the paper-sized linear problem, and for every shape split
+    widths that leave an even number of feature blocks per workgroup, a tail
+    exactly the tiles after the last full round, and at most one round of
+    workgroups in a tail launch; EINVAL (plan untouched) outside the range."""
     L = P.lib()
+    plan = (ctypes.c_int64 * 3)(-5, -5, -5)
     for args in [(1, 64, 0, 0), (256, 0, 0, 0), (256, 64, 9, 0), (256, 64, 0, 3),
                  ((1 << 22) + 1, 64, 0, 0), (256, (1 << 21) + 1, 1, 0)]:
-        assert L.lssvm_tile_split(*args) == 0, args
-    for dtype in (0, 1):
-        bk = 16 if dtype == 0 else 32
-        for kernel in (1, 2):
-            for n, d in [(2, 1), (4096, 1024), (32768, 4096)]:
-                assert L.lssvm_tile_split(n, d, dtype, kernel) == 1
-        assert L.lssvm_tile_split(32768, 4096, dtype, 0) == 1
-        assert L.lssvm_tile_split(16384, 2048, dtype, 0) == 1
-        assert L.lssvm_tile_split(4096, 1024, dtype, 0) > 1
-        for n in (2, 129, 600, 1000, 2000, 4096, 6000, 8192, 12000):
-            for d in (1, 7, 64, 100, 256, 1024, 4096):
-                S = L.lssvm_tile_split(n, d, dtype, 0)
-                nkb = -(-d // (2 * bk)) * 2
-                assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, (n, d, dtype, S)
+        assert L.lssvm_tile_plan(*args, plan) == B.EINVAL, args
+        assert list(plan) == [-5, -5, -5]
+    assert L.lssvm_tile_plan(256, 64, 0, 0, None) == B.EINVAL
+    pins = {("f64", "linear", 4096, 1024): (1, 16, 32),
+            ("f64", "linear", 16384, 4096): (1, 64, 8),
+            ("f64", "rbf", 16384, 2048): (1, 64, 8),
+            ("f32", "poly", 32768, 4096): (1, 128, 4),
+            ("f32", "rbf", 65536, 1024): (1, 0, 1),
+            ("f32", "rbf", 32768, 256): (1, 128, 4)}
+    for (dtype, kernel, n, d), want in pins.items():
+        assert P.tile_plan(n, d, dtype, kernel) == want, (dtype, kernel, n, d)
+    for dtype in ("f64", "f32"):
+        bk = 16 if dtype == "f64" else 32
+        for kernel in ("linear", "poly", "rbf"):
+            for n in (2, 129, 600, 1000, 2000, 3000, 4096, 6000, 8192, 12000, 40000):
+                for d in (1, 7, 64, 100, 256, 1024, 4096):
+                    S, Q, T = P.tile_plan(n, d, dtype, kernel)
+                    nkb = -(-d // (2 * bk)) * 2
+                    nT = -(-(n - 1) // 128)
+                    W = nT * (nT + 1) // 2
+                    where = (dtype, kernel, n, d, S, Q, T)
+                    assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, where
+                    assert T in (1, 2, 4, 8, 16, 32, 64) and nkb % (2 * T) == 0, where
+                    if kernel != "linear":
+                        assert S == 1, where
+                    if Q == 0:
+                        assert T == S, where
+                        continue
+                    assert T > S and Q * T <= 512, where
+                    if kernel == "linear":
+                        full = W * S // 512
+                        assert full >= 1 and Q == W - full * (512 // S), where
+                    else:
+                        assert Q == W % 512 and 4 <= T <= 16, where
 
 
 def _train(n=10, d=3, dtype=0, kernel=0, params=None, C=1.0, eps=1e-3, max_iter=0,

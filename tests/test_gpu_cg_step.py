@@ -10,7 +10,7 @@ import oracle as O
 import synthdata as S
 from gpu_common import (GOLDEN, TOL_ALPHA, TOL_MV, SPLIT_SHAPES, TAIL_SHAPES, check_train,  # noqa: F401
                         data_of, golden, golden_tight, kw_of, labels_match, log, oracle_ref,
-                        random_cases, random_large_cases, rel_err, small_cfg, spec_of, tail_plan,
+                        random_cases, random_large_cases, rel_err, small_cfg, spec_of,
                         to_dev)
 
 pytestmark = pytest.mark.gpu

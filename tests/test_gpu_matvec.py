@@ -12,7 +12,7 @@ import oracle as O
 import synthdata as S
 from gpu_common import (GOLDEN, TOL_ALPHA, TOL_MV, SPLIT_SHAPES, TAIL_SHAPES, check_train,  # noqa: F401
                         data_of, golden, golden_tight, kw_of, labels_match, log, oracle_ref,
-                        random_cases, random_large_cases, rel_err, small_cfg, spec_of, tail_plan,
+                        random_cases, random_large_cases, rel_err, small_cfg, spec_of,
                         to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -37,49 +37,41 @@ def test_matvec_small_shapes(torch_dev, dtype, kernel, n, d):
     assert rel_err(out.cpu().numpy(), ref) <= TOL_MV[dtype]
 
 
-@pytest.mark.parametrize("dtype,n,d,split", SPLIT_SHAPES)
-def test_matvec_linear_feature_split(torch_dev, dtype, n, d, split):
-    torch, dev = torch_dev
-    import paper_2202_12674_amd as P
-    L = P.lib()
-    assert L.lssvm_tile_split(n, d, 0 if dtype == "f64" else 1, 0) == split
-    cfg = small_cfg("linear", dtype, n, d, C=2.0)
-    log(f"matvec split {split} {cfg.name}")
+def _check_plan_product(torch, dev, P, cfg, plan):
+    """Two probes and three unit columns (the first and the last tile of the
+    visit order, and a diagonal entry whose 1/C term comes from one split)
+    against the oracle's reduced matrix."""
+    n = cfg.n
+    log(f"matvec plan {plan} {cfg.name}")
     X, y, _, _ = data_of(cfg)
     Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
     Xd = to_dev(torch, dev, X)
     for seed in (7, 8):
         p = S.probe_vector(n - 1, cfg.np_dtype, seed=seed)
         out = P.matvec(Xd, to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg)).cpu().numpy()
-        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
-    e = np.zeros(n - 1, dtype=cfg.np_dtype)
-    e[n // 2] = 1   # one column: the diagonal entry and the 1/C term come from one split
-    out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
-    assert rel_err(out, Qt[:, n // 2]) <= TOL_MV[dtype]
+        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[cfg.dtype]
+    for j in (0, n // 2, n - 2):
+        e = np.zeros(n - 1, dtype=cfg.np_dtype)
+        e[j] = 1
+        out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
+        assert rel_err(out, Qt[:, j]) <= TOL_MV[cfg.dtype], j
+    del Qt
+
+
+@pytest.mark.parametrize("dtype,n,d,plan", SPLIT_SHAPES)
+def test_matvec_linear_feature_split(torch_dev, dtype, n, d, plan):
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    assert P.tile_plan(n, d, dtype, "linear") == plan
+    _check_plan_product(torch, dev, P, small_cfg("linear", dtype, n, d, C=2.0), plan)
 
 
 @pytest.mark.parametrize("dtype,kernel,n,d,plan", TAIL_SHAPES)
 def test_matvec_tail_split(torch_dev, dtype, kernel, n, d, plan):
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
-    assert tail_plan(n, d, dtype) == plan
-    if kernel == "linear":
-        assert P.lib().lssvm_tile_split(n, d, 0 if dtype == "f64" else 1, 0) == 1
-    cfg = small_cfg(kernel, dtype, n, d, C=2.0)
-    log(f"matvec tail {plan} {cfg.name}")
-    X, y, _, _ = data_of(cfg)
-    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), cfg.C)
-    Xd = to_dev(torch, dev, X)
-    for seed in (7, 8):
-        p = S.probe_vector(n - 1, cfg.np_dtype, seed=seed)
-        out = P.matvec(Xd, to_dev(torch, dev, p), C=cfg.C, **kw_of(cfg)).cpu().numpy()
-        assert rel_err(out, Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
-    for j in (0, n - 2):   # columns of the first and the last tile of the visit order
-        e = np.zeros(n - 1, dtype=cfg.np_dtype)
-        e[j] = 1
-        out = P.matvec(Xd, to_dev(torch, dev, e), C=cfg.C, **kw_of(cfg)).cpu().numpy()
-        assert rel_err(out, Qt[:, j]) <= TOL_MV[dtype], j
-    del Qt
+    assert P.tile_plan(n, d, dtype, kernel) == plan
+    _check_plan_product(torch, dev, P, small_cfg(kernel, dtype, n, d, C=2.0), plan)
 
 
 @pytest.mark.parametrize("kernel,dtype,n,d,C", random_cases())
