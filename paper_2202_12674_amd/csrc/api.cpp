@@ -112,13 +112,16 @@ constexpr int64_t kResidentTiles = 512;
 #ifndef LSSVM_LINEAR_TAIL
 #define LSSVM_LINEAR_TAIL 1
 #endif
+#ifndef LSSVM_LINEAR_TAIL_MAX
+#define LSSVM_LINEAR_TAIL_MAX 64
+#endif
 
 // Finer split of the linear kernel's tiles in a last partial round that
 // already runs S ways: the largest T (up to 64) with Q T within one round of
 // resident workgroups and an even number of feature blocks per share.
 inline int64_t linear_tail_split(int64_t Q, int64_t S, int64_t nkb) {
   int64_t T = S;
-  while (LSSVM_LINEAR_TAIL && T < 64 && Q * T * 2 <= kResidentTiles && nkb % (4 * T) == 0)
+  while (LSSVM_LINEAR_TAIL && T < LSSVM_LINEAR_TAIL_MAX && Q * T * 2 <= kResidentTiles && nkb % (4 * T) == 0)
     T *= 2;
   return T;
 }
@@ -483,11 +486,20 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   return a;
 }
 
-// The tile visit order, written into the workspace on the device (once per call).
+#ifndef LSSVM_DIAG_TAIL
+#define LSSVM_DIAG_TAIL 1
+#endif
+
+// The tile visit order, written into the workspace on the device (once per
+// call). The linear kernel's finer-split last round takes diagonal tiles
+// where there are enough: each of its T splits then adds into one panel of
+// row sums, where the last tiles of the grouped order share a few panels
+// (up to a super-tile's worth of tiles times T atomic additions per word).
 template <typename T>
-int make_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
+int make_order(const Geometry& g, const TrainWs<T>& w, int32_t kernel, hipStream_t s) {
   if (LSSVM_TILE_GROUP <= 0 || g.nT == 0) return LSSVM_OK;
-  LSSVM_HIP(launch_tile_order(g.nT, LSSVM_TILE_GROUP, w.order, s));
+  const int64_t nd = (LSSVM_DIAG_TAIL && kernel == LSSVM_LINEAR) ? std::min(g.lin_tail_q, g.nT) : 0;
+  LSSVM_HIP(launch_tile_order(g.nT, LSSVM_TILE_GROUP, nd, w.order, s));
   return LSSVM_OK;
 }
 
@@ -497,7 +509,7 @@ int make_order(const Geometry& g, const TrainWs<T>& w, hipStream_t s) {
 template <typename T>
 int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
                  const lssvm_params& kp, hipStream_t s, bool check = true) {
-  LSSVM_TRY(make_order<T>(g, w, s));
+  LSSVM_TRY(make_order<T>(g, w, kernel, s));
   LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
   LSSVM_HIP(hipMemsetAsync(w.scal, 0, S_COUNT * sizeof(double), s));
   LSSVM_HIP(hipMemsetAsync(w.acc, 0, 2 * g.NP * sizeof(int64_t), s));

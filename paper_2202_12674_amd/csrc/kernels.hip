@@ -620,21 +620,43 @@ __global__ __launch_bounds__(256) void k_linear_scores(const T* __restrict__ Xte
 // ------------------------------------------------------------ tile order ----
 // Visit order of the upper-triangle tiles: GROUP x GROUP super-tiles column by
 // column (super-rows top down), and inside each super-tile column by column.
+// Position of tile (i, j) in that order: the tiles of the super-columns to
+// the left, the full super-tiles above it in its super-column, and the
+// columns of its super-tile before it.
+__device__ inline int64_t grouped_position(int64_t nT, int64_t G, int64_t i, int64_t j) {
+  const int64_t c0 = (j / G) * G, r0 = (i / G) * G;
+  const int64_t ncols = (nT < c0 + G ? nT : c0 + G) - c0;
+  int64_t p = c0 * (c0 + 1) / 2 + r0 * ncols;
+  for (int64_t c = c0; c < j; ++c) p += (c + 1 < r0 + G ? c + 1 : r0 + G) - r0;
+  return p + (i - r0);
+}
+
 // Thread t takes tile (i, j) of the column-major triangle and writes it,
-// packed (i << 16) | j, at its position in that order: the tiles of the
-// super-columns to the left, the full super-tiles above it in its
-// super-column, and the columns of its super-tile before it.
-__global__ __launch_bounds__(256) void k_tile_order(int64_t nT, int64_t G,
+// packed (i << 16) | j, at its position. The last nd diagonal tiles
+// (i = j >= nT - nd) move to the end of the order, the others close up:
+// a split last round made of diagonal tiles adds into nd disjoint panels,
+// one tile each, instead of into the few panels the order ends on.
+__global__ __launch_bounds__(256) void k_tile_order(int64_t nT, int64_t G, int64_t nd,
                                                     uint32_t* __restrict__ order) {
   const int64_t W = nT * (nT + 1) / 2;
   for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < W; t += (int64_t)gridDim.x * NT) {
     int64_t i, j;
     tri_index(t, i, j);
-    const int64_t c0 = (j / G) * G, r0 = (i / G) * G;
-    const int64_t ncols = (nT < c0 + G ? nT : c0 + G) - c0;
-    int64_t p = c0 * (c0 + 1) / 2 + r0 * ncols;
-    for (int64_t c = c0; c < j; ++c) p += (c + 1 < r0 + G ? c + 1 : r0 + G) - r0;
-    order[p + (i - r0)] = (uint32_t)((i << 16) | j);
+    int64_t p;
+    if (i == j && i >= nT - nd) {
+      p = W - nd + (i - (nT - nd));
+    } else {
+      // the moved tiles that came before it: diagonal positions grow with k
+      p = grouped_position(nT, G, i, j);
+      int64_t lo = nT - nd, hi = nT;   // first k in [lo, hi) placed after p
+      while (lo < hi) {
+        const int64_t mid = (lo + hi) / 2;
+        if (grouped_position(nT, G, mid, mid) < p) lo = mid + 1;
+        else hi = mid;
+      }
+      p -= lo - (nT - nd);
+    }
+    order[p] = (uint32_t)((i << 16) | j);
   }
 }
 
@@ -798,11 +820,12 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + NT - 1) / NT); }
 
 // ------------------------------------------------------------- launchers ----
 
-hipError_t launch_tile_order(int64_t nT, int64_t group, uint32_t* order, hipStream_t s) {
+hipError_t launch_tile_order(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
+                             hipStream_t s) {
   const int64_t W = nT * (nT + 1) / 2;
   const int64_t blocks = std::min<int64_t>((W + NT - 1) / NT, kVecBlocks);
   hipLaunchKernelGGL(k_tile_order, dim3((unsigned)std::max<int64_t>(1, blocks)), dim3(NT), 0, s, nT,
-                     group, order);
+                     group, diag_last, order);
   return hipGetLastError();
 }
 

@@ -103,7 +103,8 @@ constexpr int64_t kFusedMaxNP = 1024;
 
 // The symmetric tiles' visit order (GROUP x GROUP super-tiles), packed
 // (I << 16) | J, nT (nT + 1) / 2 entries.
-hipError_t launch_tile_order(int64_t nT, int64_t group, uint32_t* order, hipStream_t s);
+hipError_t launch_tile_order(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
+                             hipStream_t s);
 
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
