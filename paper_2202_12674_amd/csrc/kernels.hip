@@ -728,7 +728,9 @@ __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t
 template <typename T, int KER>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles_cg(
     TileArgs<T> a, FusedCg f) {
-  if (!tile_body<T, true, KER, kWhole>(a)) return;   // CG had already stopped
+  // vectors staged through LDS with the first block (for fp64 too): in a
+  // launch of a few workgroups the epilogue's loads would be a round trip
+  if (!tile_body<T, true, KER, kWhole, true>(a)) return;   // CG had already stopped
   __shared__ int last;
   __shared__ double sh[NT / 64];
   __threadfence();
@@ -740,27 +742,76 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   if (!last) return;
   __threadfence();
   constexpr int R = (int)(kFusedMaxNP / NT);
-  const RankOneSums ro = rank_one_sums(f.c, sh);
-  const double inv = 1.0 / f.scal[S_FIXSC];
-  const bool bad = f.c.flags[F_PRODUCT] != 0;
-  double qr[R], dr[R];
+  // Every global load of the vector step is issued here, at once: placed
+  // where it is used, each would wait for the barrier of the reduction before
+  // it and then for its own round trip, one after the other.
+  const int tid = threadIdx.x;
+  const RankOne& c = f.c;
+  const double pS = tid < c.nT ? c.pq[tid] : 0.0;
+  const double pT = tid < c.nT ? c.pq[c.nT + tid] : 0.0;
+  const double kmm = f.scal[S_KMM], fxsc = f.scal[S_FIXSC];
+  const double delta = f.scal[S_DHIST + f.par];
+  double* st = f.scal + S_STATUS;
+  const double stop = st[ST_STOP];
+  const bool bad = c.flags[F_PRODUCT] != 0;
+  int64_t lo[R], hi[R];
+  double qm[R], dr[R], xr[R], rk[R];
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    const int64_t i = tid + (int64_t)k * NT;
+    lo[k] = hi[k] = 0;
+    qm[k] = dr[k] = xr[k] = rk[k] = 0.0;
+    if (i < f.NP) {
+      lo[k] = c.acc[2 * i];
+      hi[k] = c.acc[2 * i + 1];
+      qm[k] = i < f.N ? c.q64[i] : 0.0;
+      dr[k] = f.dir[i];
+      xr[k] = f.x[i];
+      rk[k] = f.r[i];
+    }
+  }
+  // S and T of the rank-one terms (one reduction for both, each summed in
+  // the order of block_sum)
+  double S = pS, Tq = pT;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    S += __shfl_xor(S, off);
+    Tq += __shfl_xor(Tq, off);
+  }
+  {
+    __shared__ double sh2[2][NT / 64];
+    const int w = tid >> 6;
+    if ((tid & 63) == 0) {
+      sh2[0][w] = S;
+      sh2[1][w] = Tq;
+    }
+    __syncthreads();
+    S = Tq = 0.0;
+    for (int v = 0; v < NT / 64; ++v) {
+      S += sh2[0][v];
+      Tq += sh2[1][v];
+    }
+  }
+  const double qmm = kmm + c.invC, inv = 1.0 / fxsc;
+  double qr[R];
   double g = 0.0;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    const int64_t i = threadIdx.x + (int64_t)k * NT;
-    qr[k] = dr[k] = 0.0;
+    const int64_t i = tid + (int64_t)k * NT;
+    qr[k] = 0.0;
     if (i < f.NP) {
-      const double t = product_row(f.c, i, inv, bad);
-      const double q = i < f.N ? qtilde_row(f.c, ro, i, t) : 0.0;
+      c.acc[2 * i] = 0;   // cleared for the next product
+      c.acc[2 * i + 1] = 0;
+      const int64_t H2 = hi[k] + (lo[k] >> 32);   // as fixed_take
+      const double t = bad ? __builtin_nan("")
+                           : ((double)H2 * 4294967296.0 + (double)(lo[k] & 0xffffffffLL)) * inv;
+      const double q = i < f.N ? t + (qmm - qm[k]) * S - Tq + dr[k] * c.invC : 0.0;
       qr[k] = q;
-      dr[k] = f.dir[i];
       f.qv[i] = q;
       g += dr[k] * q;
     }
   }
   const double gam = block_sum(g, sh);
-  double* st = f.scal + S_STATUS;
-  const double delta = f.scal[S_DHIST + f.par];
   const double alpha = delta / gam;
   if (!(gam > 0.0) || !__builtin_isfinite(alpha)) {   // curvature breakdown: nothing moves
     if (threadIdx.x == 0) {
@@ -774,14 +825,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     return;
   }
-  double rr = 0.0, rk[R];
+  double rr = 0.0;
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    const int64_t i = threadIdx.x + (int64_t)k * NT;
-    rk[k] = 0.0;
+    const int64_t i = tid + (int64_t)k * NT;
     if (i < f.NP) {
-      f.x[i] += alpha * dr[k];
-      rk[k] = f.r[i] - alpha * qr[k];
+      f.x[i] = xr[k] + alpha * dr[k];
+      rk[k] = rk[k] - alpha * qr[k];
       f.r[i] = rk[k];
       rr += rk[k] * rk[k];
     }
@@ -809,7 +859,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     st[ST_STEP] = alpha;
     st[ST_ITER] = (double)f.iter;
     if (f.iter <= f.hist_cap) f.hist[f.iter - 1] = dnew;
-    if (dnew <= st[ST_STOP]) st[ST_DONE] = 1.0;
+    if (dnew <= stop) st[ST_DONE] = 1.0;
     *f.ticket = 0u;   // the next launch starts after this one ends
   }
 }

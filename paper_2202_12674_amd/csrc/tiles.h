@@ -185,8 +185,7 @@ __device__ inline void tri_index(int64_t t, int64_t& I, int64_t& J) {
 // kernel that reads a row (fixed_take) restores X's sum exactly and rounds it
 // once to fp64.
 template <int KER, typename T>
-__device__ inline double fixed_scale(const TileArgs<T>& a) {
-  const double pmax = a.fx[0], nmax = a.fx[1];
+__device__ inline double fixed_scale(const TileArgs<T>& a, double pmax, double nmax) {
   double km = 1.0;   // bound on |k(x_i, x_j)|: RBF values are at most 1
   if constexpr (KER == KLIN) {
     km = nmax;       // |<x, z>| <= ||x|| ||z||
@@ -243,7 +242,7 @@ __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 //
 // The body returns false when the launch found CG already stopped (nothing
 // done), true otherwise.
-template <typename T, bool SYM, int KER, int PART>
+template <typename T, bool SYM, int KER, int PART, bool VLDS = (sizeof(T) == 4)>
 __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   using MF = Mfma<T>;
   using C = TileCfg<T>;
@@ -286,9 +285,12 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // at 64 features, 0.5% at 4096). p over rows I and over columns J
   // (symmetric mode) go to vp; the squared norms of both panels (radial
   // kernel) and the column weights (general mode) to vt[0], vt[1], vt[2].
-  // fp64 reads them from global memory: staged, it measured 0.5-4% slower.
-  constexpr bool kVecLds = sizeof(T) == 4;
+  // fp64 reads them from global memory: staged, it measured 0.5-4% slower,
+  // except in a launch of one small round, where the epilogue's loads are a
+  // round trip of their own (VLDS).
+  constexpr bool kVecLds = VLDS;
   __shared__ __attribute__((aligned(16))) double vp[SYM ? 2 : 1][BM];
+  __shared__ __attribute__((aligned(16))) double vq[SYM ? BM : 1];   // q over panel I (diagonal)
   __shared__ __attribute__((aligned(16))) T vt[3][BM];
 
   if constexpr (SYM) {
@@ -344,6 +346,13 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // of each direct load (M0) needs no per-load read-back from a vector register
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  // the bounds behind the fixed-point scale, read now: in the epilogue the
+  // read would add a round trip after the last block
+  double fx_pmax = 0.0, fx_nmax = 0.0;
+  if constexpr (SYM) {
+    fx_pmax = a.fx[0];
+    fx_nmax = a.fx[1];
+  }
 
   // panel I is a.nkb consecutive blocks of BM * BK elements; this workgroup
   // contracts blocks [ks nkb, (ks + 1) nkb) of it
@@ -396,10 +405,13 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
     constexpr int TL = BM * (int)sizeof(T) / 16;   // lanes per T vector
     constexpr int TE = 16 / (int)sizeof(T);        // T entries per lane
     if constexpr (SYM) {
-      if (wave == 0)
+      if (wave == 0) {
         __builtin_amdgcn_global_load_lds((gptr_t)(a.pv + I * BM + 2 * lane), (lptr_t)&vp[0][0],
                                          16, 0, 0);
-      else if (wave == 1)
+        if (I == J && ks == 0)   // the diagonal tile's rank-one share needs q as well
+          __builtin_amdgcn_global_load_lds((gptr_t)(a.q64 + I * BM + 2 * lane), (lptr_t)&vq[0],
+                                           16, 0, 0);
+      } else if (wave == 1)
         __builtin_amdgcn_global_load_lds((gptr_t)(a.pv + J * BM + 2 * lane), (lptr_t)&vp[1][0],
                                          16, 0, 0);
     } else {
@@ -542,7 +554,7 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   const bool diag = SYM && (I == J);
   double fxs = 1.0;   // fixed-point scale of the row sums (symmetric mode)
   if constexpr (SYM) {
-    fxs = fixed_scale<KER>(a);
+    fxs = fixed_scale<KER>(a, fx_pmax, fx_nmax);
     if (blockIdx.x == 0 && tid == 0) a.fx[2] = fxs;   // every workgroup finds the same
   }
   T nBj[CB];
@@ -666,7 +678,7 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
       if (tid < BM) {
         const int64_t j = I * BM + tid;
         sp = kVecLds ? vp[0][tid] : a.pv[j];
-        sq = a.q64[j] * sp;
+        sq = (kVecLds ? vq[tid] : a.q64[j]) * sp;
       }
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
