@@ -224,6 +224,9 @@ constexpr int kBufferWord3 = 0x00020000;
 // global -> LDS loads) have completed: s_waitcnt vmcnt(0), other counters free.
 __device__ inline void vm_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// The stop flag of launches that have none (a product outside CG).
+__device__ const double kNeverStop = 0.0;
+
 // ---------------------------------------------------------- a4 tiles --------
 // One T x T tile of the pairwise contraction G = X_I X_J^T per workgroup,
 // feature blocks of BK staged global -> LDS (double-buffered) and fed to the
@@ -293,8 +296,13 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   __shared__ __attribute__((aligned(16))) double vq[SYM ? BM : 1];   // q over panel I (diagonal)
   __shared__ __attribute__((aligned(16))) T vt[3][BM];
 
+  // CG already stopped? A whole or partial tile reads the flag with its
+  // first loads in flight: waiting for it first would add a round trip to
+  // every product of a small problem.
+  double stop_v = 0.0;
   if constexpr (SYM) {
-    if (a.stop && *a.stop != 0.0) return false;   // CG already stopped
+    stop_v = *(a.stop ? a.stop : &kNeverStop);
+    if (PART == kFixup && stop_v != 0.0) return false;
   }
   int64_t I, J;
   // Symmetric tiles may have their features split over KS workgroups. For
@@ -481,6 +489,11 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   if constexpr (PART != kFixup) {
   dload(0, As0, Bs0);
   if constexpr (PART == kWhole) dvec();
+  __builtin_amdgcn_sched_barrier(0);   // the flag is tested only behind the loads
+  if (stop_v != 0.0) {   // uniform: the loads land in LDS before the workgroup ends
+    vm_wait_all();
+    return false;
+  }
   vm_wait_all();
   __syncthreads();
   for (int64_t kb = 0; kb < nkb; kb += 2) {
