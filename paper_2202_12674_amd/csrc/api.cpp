@@ -495,11 +495,13 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
 // where there are enough: each of its T splits then adds into one panel of
 // row sums, where the last tiles of the grouped order share a few panels
 // (up to a super-tile's worth of tiles times T atomic additions per word).
+// The same launch zeroes the flags, the scalars and the row-sum words.
 template <typename T>
-int make_order(const Geometry& g, const TrainWs<T>& w, int32_t kernel, hipStream_t s) {
-  if (LSSVM_TILE_GROUP <= 0 || g.nT == 0) return LSSVM_OK;
+int clear_and_order(const Geometry& g, const TrainWs<T>& w, int32_t kernel, hipStream_t s) {
+  const bool ordered = LSSVM_TILE_GROUP > 0 && g.nT > 0;
   const int64_t nd = (LSSVM_DIAG_TAIL && kernel == LSSVM_LINEAR) ? std::min(g.lin_tail_q, g.nT) : 0;
-  LSSVM_HIP(launch_tile_order(g.nT, LSSVM_TILE_GROUP, nd, w.order, s));
+  LSSVM_HIP(launch_setup_clear(g.nT, LSSVM_TILE_GROUP, nd, ordered ? w.order : nullptr, w.flags,
+                               w.scal, w.acc, 2 * g.NP, w.ticket, s));
   return LSSVM_OK;
 }
 
@@ -509,10 +511,7 @@ int make_order(const Geometry& g, const TrainWs<T>& w, int32_t kernel, hipStream
 template <typename T>
 int setup_points(const Geometry& g, const TrainWs<T>& w, const T* X, int32_t kernel,
                  const lssvm_params& kp, hipStream_t s, bool check = true) {
-  LSSVM_TRY(make_order<T>(g, w, kernel, s));
-  LSSVM_HIP(hipMemsetAsync(w.flags, 0, F_COUNT * sizeof(int), s));
-  LSSVM_HIP(hipMemsetAsync(w.scal, 0, S_COUNT * sizeof(double), s));
-  LSSVM_HIP(hipMemsetAsync(w.acc, 0, 2 * g.NP * sizeof(int64_t), s));
+  LSSVM_TRY(clear_and_order<T>(g, w, kernel, s));
   LSSVM_HIP(launch_layout<T>(X, g.n, g.d, w.Xt, g.ld, g.d_pad, w.flags, s));
   LSSVM_HIP(launch_norms_q<T>(w.Xt, g.ld, g.d_pad, g.N, g.N, kernel, kp.gamma, kp.coef0,
                               kp.degree, w.norms, w.q64, w.scal, s));
@@ -625,13 +624,14 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   LSSVM_TRY(setup_points<T>(g, w, X, kernel, kp, s, /*check=*/false));
   LSSVM_HIP(launch_rhs_init<T>(y, g.N, g.NP, w.rhs, w.x, w.xbest, w.r, w.dir, w.bp0, w.flags,
                                w.scal, s));
-  LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, s));
-  LSSVM_HIP(hipMemcpyAsync(g_ctx->flags, w.flags, F_COUNT * sizeof(int), hipMemcpyDeviceToHost,
-                           s));
-  LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_DELTA0, sizeof(double), hipMemcpyDeviceToHost, s));
+  LSSVM_HIP(launch_finish_delta0(w.bp0, g.nb, w.scal, eps * eps, w.flags, s));
+  // one read-back: r0^T r0 and the input flags
+  LSSVM_HIP(hipMemcpyAsync(g_ctx->p, w.scal + S_DELTA0, (S_INFLAGS - S_DELTA0 + 1) * sizeof(double),
+                           hipMemcpyDeviceToHost, s));
   LSSVM_HIP(hipStreamSynchronize(s));
-  if (g_ctx->flags[F_NONFINITE]) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
-  if (g_ctx->flags[F_BADLABEL]) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
+  const double inflags = g_ctx->p[S_INFLAGS - S_DELTA0];
+  if (inflags == 1.0 || inflags == 3.0) return fail(LSSVM_ENONFINITE, "X holds a NaN or an infinity");
+  if (inflags == 2.0) return fail(LSSVM_EBADLABEL, "labels must be +1 or -1");
   const double delta0 = g_ctx->p[0];
   const double t_setup = ms_since(t0);
   MatvecTimer tm;
@@ -679,7 +679,6 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
   int64_t it_prev = 0, need = max_iter;
   double delta_prev = delta;
   const bool fused = fused_iteration(g, kernel);
-  if (fused && !done) LSSVM_HIP(hipMemsetAsync(w.ticket, 0, sizeof(unsigned), s));
   // A fused iteration takes ~15 us and a status read-back ~30 us: small
   // problems start with 8 iterations queued (those run past the stop return at
   // once, a few microseconds each)

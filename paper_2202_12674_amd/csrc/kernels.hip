@@ -238,10 +238,12 @@ __global__ __launch_bounds__(256) void k_rhs_init(const T* __restrict__ y, int64
 }
 
 __global__ __launch_bounds__(256) void k_finish_delta0(const double* bpart, int64_t nb,
-                                                       double* scal, double eps2) {
+                                                       double* scal, double eps2,
+                                                       const int* flags) {
   __shared__ double sh[NT / 64];
   const double s = sum_partials(bpart, nb, sh);
   if (threadIdx.x == 0) {
+    scal[S_INFLAGS] = (flags[F_NONFINITE] ? 1.0 : 0.0) + (flags[F_BADLABEL] ? 2.0 : 0.0);
     scal[S_DELTA0] = s;
     scal[S_DHIST + 0] = s;
     double* st = scal + S_STATUS;
@@ -636,10 +638,21 @@ __device__ inline int64_t grouped_position(int64_t nT, int64_t G, int64_t i, int
 // (i = j >= nT - nd) move to the end of the order, the others close up:
 // a split last round made of diagonal tiles adds into nd disjoint panels,
 // one tile each, instead of into the few panels the order ends on.
-__global__ __launch_bounds__(256) void k_tile_order(int64_t nT, int64_t G, int64_t nd,
-                                                    uint32_t* __restrict__ order) {
+// The same launch zeroes the flags, the scalars and the row-sum words.
+__global__ __launch_bounds__(256) void k_setup_clear(int64_t nT, int64_t G, int64_t nd,
+                                                     uint32_t* __restrict__ order,
+                                                     int* __restrict__ flags,
+                                                     double* __restrict__ scal,
+                                                     int64_t* __restrict__ acc, int64_t nacc,
+                                                     unsigned* __restrict__ ticket) {
+  const int64_t t0 = (int64_t)blockIdx.x * NT + threadIdx.x, stride = (int64_t)gridDim.x * NT;
+  if (t0 < F_COUNT) flags[t0] = 0;
+  if (t0 == 0 && ticket) *ticket = 0u;
+  if (t0 < S_COUNT) scal[t0] = 0.0;
+  for (int64_t t = t0; t < nacc; t += stride) acc[t] = 0;
+  if (!order) return;
   const int64_t W = nT * (nT + 1) / 2;
-  for (int64_t t = (int64_t)blockIdx.x * NT + threadIdx.x; t < W; t += (int64_t)gridDim.x * NT) {
+  for (int64_t t = t0; t < W; t += stride) {
     int64_t i, j;
     tri_index(t, i, j);
     int64_t p;
@@ -875,12 +888,14 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + NT - 1) / NT); }
 
 // ------------------------------------------------------------- launchers ----
 
-hipError_t launch_tile_order(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
-                             hipStream_t s) {
-  const int64_t W = nT * (nT + 1) / 2;
-  const int64_t blocks = std::min<int64_t>((W + NT - 1) / NT, kVecBlocks);
-  hipLaunchKernelGGL(k_tile_order, dim3((unsigned)std::max<int64_t>(1, blocks)), dim3(NT), 0, s, nT,
-                     group, diag_last, order);
+hipError_t launch_setup_clear(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
+                              int* flags, double* scal, int64_t* acc, int64_t nacc,
+                              unsigned* ticket, hipStream_t s) {
+  const int64_t W = order ? nT * (nT + 1) / 2 : 0;
+  const int64_t n = std::max<int64_t>(std::max<int64_t>(W, nacc), S_COUNT);
+  const int64_t blocks = std::min<int64_t>((n + NT - 1) / NT, kVecBlocks);
+  hipLaunchKernelGGL(k_setup_clear, dim3((unsigned)std::max<int64_t>(1, blocks)), dim3(NT), 0, s,
+                     nT, group, diag_last, order, flags, scal, acc, nacc, ticket);
   return hipGetLastError();
 }
 
@@ -993,8 +1008,8 @@ hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, doubl
 }
 
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
-                                hipStream_t s) {
-  hipLaunchKernelGGL(k_finish_delta0, dim3(1), dim3(NT), 0, s, bpart, nb, scal, eps2);
+                                const int* flags, hipStream_t s) {
+  hipLaunchKernelGGL(k_finish_delta0, dim3(1), dim3(NT), 0, s, bpart, nb, scal, eps2, flags);
   return hipGetLastError();
 }
 

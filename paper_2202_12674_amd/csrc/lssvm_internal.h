@@ -45,6 +45,8 @@ enum Scalar : int {
   S_PMAX = 20,
   S_NMAX = 21,
   S_FIXSC = 22,
+  S_INFLAGS = 23,   // the input flags as read after the right-hand side: 1 non-finite
+                    // X, 2 a label other than +-1 (one read-back with S_DELTA0)
   S_COUNT = 24
 };
 enum StatusField : int { ST_DELTA = 0, ST_CURV = 1, ST_STEP = 2, ST_ITER = 3, ST_DONE = 4,
@@ -103,8 +105,13 @@ constexpr int64_t kFusedMaxNP = 1024;
 
 // The symmetric tiles' visit order (GROUP x GROUP super-tiles), packed
 // (I << 16) | J, nT (nT + 1) / 2 entries.
-hipError_t launch_tile_order(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
-                             hipStream_t s);
+// The first kernel of a training: zeroes the flags (F_COUNT ints), the
+// scalars (S_COUNT doubles), the row-sum words (nacc int64) and the fused
+// iteration's ticket (if given), and writes the tile visit order (order may
+// be null: then nothing but the zeroing).
+hipError_t launch_setup_clear(int64_t nT, int64_t group, int64_t diag_last, uint32_t* order,
+                              int* flags, double* scal, int64_t* acc, int64_t nacc,
+                              unsigned* ticket, hipStream_t s);
 
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
@@ -139,7 +146,7 @@ hipError_t launch_rhs_init(const T* y, int64_t N, int64_t NP, double* rhs, doubl
 // CG kernels: once the status says done, every later kernel of the queue
 // returns at once, so the host may enqueue iterations ahead of the test.
 hipError_t launch_finish_delta0(const double* bpart, int64_t nb, double* scal, double eps2,
-                                hipStream_t s);
+                                const int* flags, hipStream_t s);
 // q = Q~ dir (c.p = dir) and the block partials of dir^T q.
 hipError_t launch_cg_gather(const RankOne& c, int64_t NP, int64_t N, double* qv, double* bpart,
                             hipStream_t s);
