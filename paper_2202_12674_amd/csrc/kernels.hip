@@ -741,9 +741,7 @@ __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t
 template <typename T, int KER>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles_cg(
     TileArgs<T> a, FusedCg f) {
-  // vectors staged through LDS with the first block (for fp64 too): in a
-  // launch of a few workgroups the epilogue's loads would be a round trip
-  if (!tile_body<T, true, KER, kWhole, true>(a)) return;   // CG had already stopped
+  if (!tile_body<T, true, KER, kWhole>(a)) return;   // CG had already stopped
   __shared__ int last;
   __shared__ double sh[NT / 64];
   // Every wave releases its own writes (row sums, rank-one partials) at agent

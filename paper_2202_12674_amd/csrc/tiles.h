@@ -245,7 +245,7 @@ __device__ const double kNeverStop = 0.0;
 //
 // The body returns false when the launch found CG already stopped (nothing
 // done), true otherwise.
-template <typename T, bool SYM, int KER, int PART, bool VLDS = (sizeof(T) == 4)>
+template <typename T, bool SYM, int KER, int PART>
 __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   using MF = Mfma<T>;
   using C = TileCfg<T>;
@@ -282,16 +282,13 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   __shared__ __attribute__((aligned(16))) T Bs1[CHUNKS * VEC];
   __shared__ double red_r[WAVES_N][BM];
   __shared__ double red_c[WAVES_M][BM];
-  // fp32: the tile's panel vectors are staged with its first feature block,
-  // so the epilogue reads no global memory (its loads of p and the norms
-  // otherwise cost several L2 round trips per tile: up to 10% of the product
-  // at 64 features, 0.5% at 4096). p over rows I and over columns J
-  // (symmetric mode) go to vp; the squared norms of both panels (radial
+  // The tile's panel vectors are staged with its first feature block, so the
+  // epilogue reads no global memory (its loads of p and the norms otherwise
+  // cost several L2 round trips per tile: up to 10% of the product at 64
+  // features, 0.5% at 4096 in fp32; in fp64 ~1% at 1024 and 2048 features).
+  // p over rows I and over columns J (symmetric mode) go to vp, q over panel
+  // I to vq (diagonal tiles); the squared norms of both panels (radial
   // kernel) and the column weights (general mode) to vt[0], vt[1], vt[2].
-  // fp64 reads them from global memory: staged, it measured 0.5-4% slower,
-  // except in a launch of one small round, where the epilogue's loads are a
-  // round trip of their own (VLDS).
-  constexpr bool kVecLds = VLDS;
   __shared__ __attribute__((aligned(16))) double vp[SYM ? 2 : 1][BM];
   __shared__ __attribute__((aligned(16))) double vq[SYM ? BM : 1];   // q over panel I (diagonal)
   __shared__ __attribute__((aligned(16))) T vt[3][BM];
@@ -409,7 +406,6 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // a T vector of 128 entries with lanes beyond it idle. Every vector is
   // padded to whole panels, so the pieces stay inside it.
   auto dvec = [&]() {
-    if constexpr (!kVecLds) return;
     constexpr int TL = BM * (int)sizeof(T) / 16;   // lanes per T vector
     constexpr int TE = 16 / (int)sizeof(T);        // T entries per lane
     if constexpr (SYM) {
@@ -478,14 +474,13 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // ends the iteration which last read it. The host pads the features to an
   // even number of blocks, so both halves of the loop body always run.
   //
-  // Scheduling fences, chosen by measurement per element type: left alone,
-  // the compiler sinks the fp32 block loads into the last quarter of the
-  // compute (less time to hide them) and hoists the fp64 wait and barrier
-  // above the last MFMAs of the block (the wave then stalls with work
-  // unissued). Pinning the loads above the compute gains ~0.5% for fp32;
-  // keeping the wait behind every MFMA gains ~5% for fp64 (the other fence
-  // costs each type a little).
-  constexpr bool kPinLoads = sizeof(T) == 4, kPinWait = sizeof(T) == 8;
+  // Scheduling fence, chosen by measurement: left alone, the compiler sinks
+  // the fp32 block loads into the last quarter of the compute (less time to
+  // hide them); pinning them above it gains ~0.5%. fp64 runs unfenced: with
+  // the earlier per-lane-address loads, keeping its wait behind every MFMA
+  // gained ~5%, with the buffer loads the fence costs ~1% (16384 x 2048 RBF,
+  // 16384 x 1024 cubic) and pinning the fp64 loads costs 1% too.
+  constexpr bool kPinLoads = sizeof(T) == 4;
   if constexpr (PART != kFixup) {
   dload(0, As0, Bs0);
   if constexpr (PART == kWhole) dvec();
@@ -500,13 +495,11 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
     dload(kb + 1, As1, Bs1);
     if constexpr (kPinLoads) __builtin_amdgcn_sched_barrier(0);
     compute(As0, Bs0);
-    if constexpr (kPinWait) __builtin_amdgcn_sched_barrier(0);
     vm_wait_all();     // this wave's part of block kb + 1 has landed
     __syncthreads();   // every wave's part has landed; stage 0 is free
     if (kb + 2 < nkb) dload(kb + 2, As0, Bs0);
     if constexpr (kPinLoads) __builtin_amdgcn_sched_barrier(0);
     compute(As1, Bs1);
-    if constexpr (kPinWait) __builtin_amdgcn_sched_barrier(0);
     vm_wait_all();
     __syncthreads();
   }
@@ -538,11 +531,9 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
           }
       return true;
     } else {
-      if constexpr (kVecLds) {
-        dvec();
-        vm_wait_all();
-        __syncthreads();
-      }
+      dvec();
+      vm_wait_all();
+      __syncthreads();
       for (int64_t s2 = 0; s2 < KS; ++s2) {
 #pragma unroll
         for (int i = 0; i < RB; ++i)
@@ -575,10 +566,9 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
     const int lj = wn * C::WN + j * MF::M + cl;
-    const int64_t gj = J * BM + lj;
-    nBj[j] = (KER == KRBF) ? (kVecLds ? vt[1][lj] : a.nB[gj]) : T(0);
-    if constexpr (SYM) pBj[j] = kVecLds ? vp[1][lj] : a.pv[gj];
-    else pBj[j] = kVecLds ? (double)vt[2][lj] : (double)a.wB[gj];
+    nBj[j] = (KER == KRBF) ? vt[1][lj] : T(0);
+    if constexpr (SYM) pBj[j] = vp[1][lj];
+    else pBj[j] = (double)vt[2][lj];
   }
   double cs[CB];
 #pragma unroll
@@ -600,9 +590,8 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
 #pragma unroll
     for (int vv = 0; vv < VH; ++vv) {
       const int li = wm * C::WM + i * MF::M + MF::row(v0 + vv, lane);
-      const int64_t gi = I * BM + li;
-      const T nAi = (KER == KRBF) ? (kVecLds ? vt[0][li] : a.nA[gi]) : T(0);
-      pAi[vv] = SYM ? (kVecLds ? vp[0][li] : a.pv[gi]) : 0.0;
+      const T nAi = (KER == KRBF) ? vt[0][li] : T(0);
+      pAi[vv] = SYM ? vp[0][li] : 0.0;
 #pragma unroll
       for (int j = 0; j < CB; ++j)
         kv[vv][j] = kernel_value<KER, T>(acc[i][j][v0 + vv], nAi, nBj[j], a.gamma, a.coef0,
@@ -689,9 +678,8 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
       __shared__ double red_d[PW][2];
       double sp = 0.0, sq = 0.0;
       if (tid < BM) {
-        const int64_t j = I * BM + tid;
-        sp = kVecLds ? vp[0][tid] : a.pv[j];
-        sq = (kVecLds ? vq[tid] : a.q64[j]) * sp;
+        sp = vp[0][tid];
+        sq = vq[tid] * sp;
       }
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
