@@ -131,68 +131,119 @@ __device__ inline double product_row(const RankOne& c, int64_t i, double inv_sca
 // A tile therefore streams one contiguous run of memory per panel (few pages,
 // coalesced), and each point's features in a block are contiguous (wide LDS
 // reads). Zero fill beyond n points and d features.
+//
+// One workgroup moves one slab b = pb * nkb + kb (TP points x BK features,
+// 16 KiB) as 16-byte chunks, PER per thread, all loads issued before the
+// stores: chunk c of the slab is point c / CPR's features (c % CPR) VEC ..,
+// a 16-byte piece of one input row, so the lanes of a load instruction read
+// whole 128-byte row segments and the stores are one contiguous run. With
+// vec_ok (d a multiple of VEC and X 16-byte aligned) a chunk is one vector
+// load; otherwise each element is loaded on its own.
 template <typename T, int BK, int TP>
 __global__ __launch_bounds__(256) void k_layout(const T* __restrict__ X, int64_t n, int64_t d,
-                                                T* __restrict__ Xb, int64_t ld, int64_t nkb,
-                                                int* __restrict__ flags) {
-  const int64_t total = nkb * ld * BK;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * 256) {
-    const int64_t kk = idx % BK;
-    const int64_t r = (idx / BK) % TP;
-    const int64_t kb = (idx / ((int64_t)BK * TP)) % nkb;
-    const int64_t pb = idx / ((int64_t)BK * TP * nkb);
-    const int64_t i = pb * TP + r, k = kb * BK + kk;
-    T v = T(0);
-    if (i < n && k < d) {
-      v = X[i * d + k];
-      if (!__builtin_isfinite(v)) flags[F_NONFINITE] = 1;
+                                                T* __restrict__ Xb, int64_t nslab, int64_t nkb,
+                                                int vec_ok, int* __restrict__ flags) {
+  constexpr int VEC = 16 / (int)sizeof(T), CPR = BK / VEC, PER = TP * CPR / 256;
+  static_assert(TP * CPR % 256 == 0, "a slab splits evenly over 256 threads");
+  typedef T vec_t __attribute__((ext_vector_type(VEC)));
+  for (int64_t b = blockIdx.x; b < nslab; b += gridDim.x) {
+    const int64_t pb = b / nkb, kb = b - pb * nkb;
+    vec_t v[PER];
+    bool bad = false;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = u * 256 + (int)threadIdx.x;
+      const int64_t i = pb * TP + c / CPR, k = kb * BK + (c % CPR) * VEC;
+      if (vec_ok) {
+        if (i < n && k < d) {
+          v[u] = *reinterpret_cast<const vec_t*>(X + i * d + k);
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) v[u][e] = T(0);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[u][e] = (i < n && k + e < d) ? X[i * d + k + e] : T(0);
+      }
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) bad |= !__builtin_isfinite(v[u][e]);
     }
-    Xb[idx] = v;
+    T* dst = Xb + b * TP * BK;
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      *reinterpret_cast<vec_t*>(dst + (u * 256 + (int)threadIdx.x) * VEC) = v[u];
+    if (bad) flags[F_NONFINITE] = 1;
   }
 }
 
 // ----------------------------------------------------------- a2 norms, q ----
-// One thread per point: ||x_i||^2 and, if a pivot m is given, the cached
-// q_i = k(x_i, x_m) for i < N (zero beyond) and k(x_m, x_m). fp64 sums.
+// Threads per point of k_norms_q: two lane groups (even and odd feature
+// blocks) of one thread per 16-byte chunk of a point's block row.
+template <typename T>
+constexpr int norms_threads_per_point() {
+  return 2 * (TileShape<T>::BK * (int)sizeof(T) / 16);
+}
+
+// ||x_i||^2 and, if a pivot m is given, the cached q_i = k(x_i, x_m) for
+// i < N (zero beyond) and k(x_m, x_m). fp64 sums. A workgroup takes PPB
+// points, KSPL x CPR threads per point: each thread sums one 16-byte chunk of
+// the point's row in every KSPL-th feature block (a wave reads whole 128-byte
+// rows), and the point's partial sums are then combined over its lanes (xor
+// 1, 2, 4, 8: a fixed order).
 template <typename T, int BK, int TP, int KER>
 __global__ __launch_bounds__(256) void k_norms_q(const T* __restrict__ Xb, int64_t ld,
                                                  int64_t nkb, int64_t m, int64_t N, double gamma,
                                                  double coef0, int degree, T* __restrict__ norms,
                                                  double* __restrict__ q64,
                                                  double* __restrict__ scal) {
+  constexpr int VEC = 16 / (int)sizeof(T), CPR = BK / VEC, KSPL = 2, TPP = KSPL * CPR;
+  static_assert(TPP == norms_threads_per_point<T>() && BK == TileShape<T>::BK, "launch shape");
+  constexpr int PPB = 256 / TPP;
+  static_assert(TP % PPB == 0, "a workgroup's points lie in one panel");
+  typedef T vec_t __attribute__((ext_vector_type(VEC)));
   __shared__ double sh[NT / 64];
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
-  double nrm = 0.0;
-  if (i < ld) {
-    double dot = 0.0, dist = 0.0;
-    const T* pi = Xb + ((i / TP) * nkb * TP + i % TP) * BK;   // point i, block 0
-    const T* pm = m >= 0 ? Xb + ((m / TP) * nkb * TP + m % TP) * BK : pi;   // pivot, block 0
-    for (int64_t kb = 0; kb < nkb; ++kb) {
-      const T* xi = pi + kb * TP * BK;            // this point's BK features (padding is 0)
-      if (m >= 0) {
-        const T* xm = pm + kb * TP * BK;
+  const int q = (int)threadIdx.x % CPR, h = ((int)threadIdx.x / CPR) % KSPL;
+  const int64_t i = (int64_t)blockIdx.x * PPB + (int64_t)threadIdx.x / TPP;   // < ld
+  const int64_t bstride = (int64_t)TP * BK;   // elements between a point's feature blocks
+  const T* pi = Xb + ((i / TP) * nkb * TP + i % TP) * BK + q * VEC;
+  double nrm = 0.0, dot = 0.0, dist = 0.0;
+  if (m >= 0) {
+    const T* pm = Xb + ((m / TP) * nkb * TP + m % TP) * BK + q * VEC;
+#pragma unroll 4
+    for (int64_t kb = h; kb < nkb; kb += KSPL) {
+      const vec_t xi = *reinterpret_cast<const vec_t*>(pi + kb * bstride);
+      const vec_t xm = *reinterpret_cast<const vec_t*>(pm + kb * bstride);
 #pragma unroll
-        for (int kk = 0; kk < BK; ++kk) {
-          const double xv = (double)xi[kk], xw = (double)xm[kk];
-          nrm += xv * xv;
-          dot += xv * xw;
-          const double df = xv - xw;
-          dist += df * df;
-        }
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < BK; ++kk) {
-          const double xv = (double)xi[kk];
-          nrm += xv * xv;
-        }
+      for (int e = 0; e < VEC; ++e) {
+        const double xv = (double)xi[e], xw = (double)xm[e];
+        nrm += xv * xv;
+        dot += xv * xw;
+        const double df = xv - xw;
+        dist += df * df;
       }
     }
+  } else {
+#pragma unroll 4
+    for (int64_t kb = h; kb < nkb; kb += KSPL) {
+      const vec_t xi = *reinterpret_cast<const vec_t*>(pi + kb * bstride);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const double xv = (double)xi[e];
+        nrm += xv * xv;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < TPP; off <<= 1) {
+    nrm += __shfl_xor(nrm, off);
+    dot += __shfl_xor(dot, off);
+    dist += __shfl_xor(dist, off);
+  }
+  if (q == 0 && h == 0) {
     norms[i] = (T)nrm;
     if (m >= 0) {
       const double kv = kernel_value64<KER>(dot, dist, gamma, coef0, degree);
-      const double qv = i < N ? kv : 0.0;
-      q64[i] = qv;
+      q64[i] = i < N ? kv : 0.0;
       if (i == m) scal[S_KMM] = kv;
     }
   }
@@ -701,12 +752,24 @@ __global__ __launch_bounds__(256) void k_predict_finish(const double* __restrict
                                                         int32_t* __restrict__ labels,
                                                         const int* __restrict__ flags) {
   if (flags[F_NONFINITE] != 0) return;   // outputs untouched on error
-  const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
+  // 64 test points per workgroup: wave w sums slots w, w + 4, ... (eight
+  // loads in flight per lane), then the four wave sums are added in order.
+  __shared__ double sh[NT / 64][64];
+  const int w = (int)threadIdx.x >> 6, l = (int)threadIdx.x & 63;
+  const int64_t i = (int64_t)blockIdx.x * 64 + l;
+  double s = 0.0;
   if (i < n_test) {
-    double s = b;
-    for (int64_t sl = 0; sl < nslots; ++sl) s += part[sl * ld + i];
-    scores[i] = (T)s;
-    if (labels) labels[i] = s > 0.0 ? 1 : -1;
+#pragma unroll 8
+    for (int64_t sl = w; sl < nslots; sl += NT / 64) s += part[sl * ld + i];
+  }
+  sh[w][l] = s;
+  __syncthreads();
+  if (w == 0 && i < n_test) {
+    double f = b;
+#pragma unroll
+    for (int v = 0; v < NT / 64; ++v) f += sh[v][l];
+    scores[i] = (T)f;
+    if (labels) labels[i] = f > 0.0 ? 1 : -1;
   }
 }
 
@@ -900,12 +963,13 @@ hipError_t launch_setup_clear(int64_t nT, int64_t group, int64_t diag_last, uint
 template <typename T>
 hipError_t launch_layout(const T* X, int64_t n, int64_t d, T* Xt, int64_t ld, int64_t d_pad,
                          int* flags, hipStream_t s) {
-  constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
-  const int64_t total = d_pad * ld;
-  // grid-stride: the element count can exceed what one dispatch can count
-  const int64_t blocks = std::min<int64_t>((total + 255) / 256, int64_t(1) << 20);
+  constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T, VEC = 16 / (int)sizeof(T);
+  const int64_t nkb = d_pad / BK, nslab = (ld / TP) * nkb;
+  const int vec_ok = d % VEC == 0 && reinterpret_cast<uintptr_t>(X) % 16 == 0;
+  // slab-stride: the slab count can exceed what one dispatch should hold
+  const int64_t blocks = std::min<int64_t>(nslab, int64_t(1) << 20);
   hipLaunchKernelGGL((k_layout<T, BK, TP>), dim3((unsigned)blocks), dim3(256), 0, s, X, n, d, Xt,
-                     ld, d_pad / BK, flags);
+                     nslab, nkb, vec_ok, flags);
   return hipGetLastError();
 }
 
@@ -915,7 +979,8 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
                           double* q64, double* scal, hipStream_t s) {
   constexpr int BK = TileShape<T>::BK, TP = TileShape<T>::T;
   const int64_t nkb = d_pad / BK;
-  const unsigned g = blocks_for(ld);
+  constexpr int PPB = 256 / norms_threads_per_point<T>();   // points per workgroup
+  const unsigned g = (unsigned)(ld / PPB);                   // ld is a multiple of TP
   switch (kernel) {
     case KLIN:
       hipLaunchKernelGGL((k_norms_q<T, BK, TP, KLIN>), dim3(g), dim3(NT), 0, s, Xt, ld, nkb, m, N,
@@ -1104,8 +1169,8 @@ template <typename T>
 hipError_t launch_predict_finish(const double* part, int64_t nslots, int64_t ld, int64_t n_test,
                                  double b, T* scores, int32_t* labels, const int* flags,
                                  hipStream_t s) {
-  hipLaunchKernelGGL(k_predict_finish<T>, dim3(blocks_for(n_test)), dim3(NT), 0, s, part, nslots,
-                     ld, n_test, b, scores, labels, flags);
+  hipLaunchKernelGGL(k_predict_finish<T>, dim3((unsigned)((n_test + 63) / 64)), dim3(NT), 0, s,
+                     part, nslots, ld, n_test, b, scores, labels, flags);
   return hipGetLastError();
 }
 
