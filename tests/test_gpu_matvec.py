@@ -254,3 +254,38 @@ def test_matvec_large_n_sampled_rows(torch_dev, dtype, kernel, n, d):
     err = float(np.abs(o[rows] - ref).max() / np.abs(ref).max())
     log(f"  {len(rows)} sampled rows: max rel err {err:.2e}")
     assert err <= TOL_MV[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f64", "f32"])
+def test_unaligned_points_match_aligned(torch_dev, dtype):
+    """Points whose start is not 16-byte aligned (a contiguous view one element
+    into a buffer) take the layout's element-wise loads; product, training and
+    prediction are bitwise those of the aligned copy, which takes its 16-byte
+    loads (d is a multiple of the vector width here)."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = small_cfg("rbf", dtype, 300, 64)
+    X, y, Xte, _ = data_of(cfg)
+    Xa = to_dev(torch, dev, X)
+    tdt = Xa.dtype
+
+    def unaligned(A):
+        buf = torch.zeros(A.size + 1, dtype=tdt, device=dev)
+        U = buf[1:].view(*A.shape)
+        U.copy_(torch.from_numpy(A).to(dev))
+        assert U.is_contiguous() and U.data_ptr() % 16 != 0
+        return U
+
+    Xu = unaligned(X)
+    p = to_dev(torch, dev, S.probe_vector(cfg.n - 1, cfg.np_dtype))
+    a = P.matvec(Xa, p, C=cfg.C, **kw_of(cfg)).cpu().numpy()
+    b = P.matvec(Xu, p, C=cfg.C, **kw_of(cfg)).cpu().numpy()
+    assert np.array_equal(a, b)
+    yd = to_dev(torch, dev, y)
+    ra = P.train(Xa, yd, C=cfg.C, eps=cfg.eps, **kw_of(cfg))
+    rb = P.train(Xu, yd, C=cfg.C, eps=cfg.eps, **kw_of(cfg))
+    assert ra.iterations == rb.iterations and ra.b == rb.b
+    assert torch.equal(ra.alpha, rb.alpha)
+    sa, la = P.predict(Xa, ra.alpha, ra.b, to_dev(torch, dev, Xte), **kw_of(cfg))
+    sb, lb = P.predict(Xu, rb.alpha, rb.b, unaligned(Xte), **kw_of(cfg))
+    assert torch.equal(sa, sb) and torch.equal(la, lb)
