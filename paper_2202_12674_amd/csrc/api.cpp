@@ -83,8 +83,8 @@ struct Geometry {
   int64_t NP;       // nT * tile: padded length of every CG vector
   int64_t nb;       // blocks of the CG vector kernels over NP (block partials per reduction)
   int64_t ksplit;   // linear kernel: workgroups per tile, each over a share of the features
-  int64_t lin_tail_q;      // linear kernel: tiles of the last partial round (or 0), in a
-  int64_t lin_tail_split;  // second launch split this many ways
+  int64_t lin_tail_q;      // linear kernel: tiles of the last partial round (or 0), run by
+  int64_t lin_tail_split;  // the launch's trailing workgroups, split this many ways
   int64_t tail_q;   // other kernels: tiles of the last partial round that are split (or 0)
   int64_t tail_split;  // ... over this many workgroups each
 };
@@ -540,11 +540,14 @@ hipError_t launch_product(const Geometry& g, TileArgs<T> a, int32_t kernel, T* g
   const int64_t W = tri_count(g.nT);
   if (kernel == LSSVM_LINEAR) {   // feature splits add up: the tail only splits finer
     const int64_t F = W - g.lin_tail_q;
-    hipError_t e = launch_tiles_sym<T>(a, kernel, kWhole, F * a.ksplit, s);
-    if (e != hipSuccess || g.lin_tail_q == 0) return e;
-    a.tile_offset = F;
-    a.ksplit = g.lin_tail_split;
-    return launch_tiles_sym<T>(a, kernel, kWhole, g.lin_tail_q * g.lin_tail_split, s);
+    if (g.lin_tail_q == 0) return launch_tiles_sym<T>(a, kernel, kWhole, F * a.ksplit, s);
+    // the finer-split last round as the launch's trailing workgroups: they
+    // start as the whole tiles finish, with no second launch to wait for
+    a.tail_slot = F * a.ksplit;
+    a.tail_split = g.lin_tail_split;
+    a.tail_tile = F;
+    return launch_tiles_sym<T>(a, kernel, kWhole,
+                               F * a.ksplit + g.lin_tail_q * g.lin_tail_split, s);
   }
   if (g.tail_q == 0) return launch_tiles_sym<T>(a, kernel, kWhole, W, s);
   const int64_t F = W - g.tail_q;

@@ -52,6 +52,12 @@ struct TileArgs {
                    // the inner product itself). Split launches park inner products in
                    // gpart instead and a fixup launch finishes each tile.
   int64_t tile_offset;  // symmetric mode: first tile of the launch in the visit order
+  // Linear kernel, whole tiles: with tail_split > 0, the workgroup slots from
+  // tail_slot on run the last round split finer in the same launch: slot
+  // tail_slot + u takes split u % tail_split of tile tail_tile + u / tail_split
+  // of the visit order (its share of the features adds into the row sums like
+  // any split's). tail_split = 0: no such slots.
+  int64_t tail_slot, tail_split, tail_tile;
   T* gpart;             // split launches: parked inner products, ksplit 128^2 per tile
   const uint32_t* order;  // symmetric mode: (I << 16) | J per visit slot, or null
   double* part;  // general mode: partial sums, part[slot * part_ld + row]

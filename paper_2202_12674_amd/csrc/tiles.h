@@ -323,16 +323,26 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   // own (the sums add up because the kernel value is the inner product
   // itself); otherwise the splits meet in the kFixup launch. Workgroup slot v
   // takes split v % KS of tile v / KS of this launch, which starts at
-  // a.tile_offset of the visit order.
-  const int64_t KS = (SYM && (KER == KLIN || PART != kWhole)) ? a.ksplit : 1;
-  int64_t ks = 0, trel = 0;
+  // a.tile_offset of the visit order; a linear launch's trailing slots run
+  // its last round split finer (a.tail_slot).
+  int64_t KS = (SYM && (KER == KLIN || PART != kWhole)) ? a.ksplit : 1;
+  int64_t ks = 0, trel = 0, first = a.tile_offset;
   const int64_t t = a.tile_base + (int64_t)blockIdx.x;   // this workgroup's slot
   if constexpr (SYM) {
-    int64_t v = t;
-    if (a.order && PART != kFixup) {
+    int64_t v = t, G = a.ntiles;
+    if (KER == KLIN && PART == kWhole && a.tail_split > 0) {
+      if (t >= a.tail_slot) {
+        KS = a.tail_split;
+        first = a.tail_tile;
+        v = t - a.tail_slot;
+        G = 0;   // no XCD runs: each tail tile adds into a panel of its own
+      } else {
+        G = a.tail_slot;
+      }
+    }
+    if (a.order && PART != kFixup && G > 0) {
       // workgroup w runs on XCD w % 8 (chunks start at multiples of 8, so this
       // holds for the slot t too): give each XCD a contiguous run of the order
-      const int64_t G = a.ntiles;
       const int64_t x = t % kNumXcd, per = G / kNumXcd, extra = G % kNumXcd;
       v = x * per + (x < extra ? x : extra) + t / kNumXcd;
     }
@@ -341,7 +351,7 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
       trel = v / KS;
       ks = v - trel * KS;
     }
-    const int64_t tile = a.tile_offset + trel;
+    const int64_t tile = first + trel;
     if (a.order) {
       const uint32_t packed = a.order[tile];
       I = packed >> 16;
