@@ -221,12 +221,16 @@ def test_matvec_rejects_nonfinite(torch_dev):
 
 
 @pytest.mark.parametrize("dtype,kernel,n,d", [("f32", "rbf", 1 << 20, 16),
-                                              ("f64", "linear", (1 << 19) + 77, 24)])
+                                              ("f64", "linear", (1 << 19) + 77, 24),
+                                              ("f64", "linear", 530000, 256)])
 def test_matvec_large_n_sampled_rows(torch_dev, dtype, kernel, n, d):
     """The implicit product at n up to 2^20 points (33.6M tiles adding into
     2^21 fixed-point words): sampled rows, including the last row and
     the ragged last tile, against the oracle's rows computed one by one; over
-    all rows, p^T Q~ p > 0 (Q~ is SPD) and every entry finite."""
+    all rows, p^T Q~ p > 0 (Q~ is SPD) and every entry finite. At 530000 x 256
+    fp64 the linear product's 8.6M tiles take two launch chunks and its last
+    round (11 tiles split 8 ways) runs as the trailing workgroups of the
+    second."""
     torch, dev = torch_dev
     import paper_2202_12674_amd as P
     log(f"[large n] {kernel} {dtype} n={n} d={d}")
