@@ -279,9 +279,10 @@ int32_t lssvm_tile_size(int32_t dtype);
  *            split over 2..16 workgroups per tile (the partial sums add up
  *            because the linear kernel value is the inner product itself);
  *   plan[1]  tiles of a last partial round that run split finer (0 if none):
- *            the linear kernel runs them in a second launch, split the same
- *            additive way; the other kernels park their partial inner
- *            products and sum them in a fix-up launch;
+ *            the linear kernel runs them as the trailing workgroups of
+ *            the same launch, split the same additive way; the other
+ *            kernels park their partial inner products and sum them in a
+ *            fix-up launch;
  *   plan[2]  workgroups per such tile (plan[0] when plan[1] is 0).
  * Every split leaves an even number of feature blocks per workgroup.
  * Returns LSSVM_EINVAL (plan untouched) for n, d, dtype or kernel out of
