@@ -117,10 +117,12 @@ typedef struct lssvm_info {
 } lssvm_info;
 
 /* Device workspace needed by lssvm_train and lssvm_matvec for n points of
- * d features. Returns 0 if n < 1, d < 1 or dtype is unknown. */
+ * d features. Returns 0 if n or d is outside the supported range (below) or
+ * dtype is unknown. */
 size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype);
 
-/* Device workspace needed by lssvm_predict. Returns 0 on bad sizes/dtype. */
+/* Device workspace needed by lssvm_predict. Returns 0 if a size is outside
+ * the supported range or dtype is unknown. */
 size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32_t dtype);
 
 /*
@@ -128,7 +130,8 @@ size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32
  *
  * X         device, n x d row-major, dtype. Must be finite.
  * y         device, n labels, dtype, each exactly +1 or -1.
- * n, d      n >= 1 points, d >= 1 features.
+ * n, d      1 <= n <= 2^22 points, 1 <= d <= 2^21 features (the supported
+ *           range of every entry point; LSSVM_EINVAL outside it).
  * kernel    LSSVM_LINEAR / LSSVM_POLY / LSSVM_RBF; kp its parameters (host, may
  *           be NULL for LSSVM_LINEAR).
  * C         regularisation, finite and > 0.
@@ -167,7 +170,8 @@ int lssvm_train(const void* X, const void* y, int64_t n, int64_t d, int32_t dtyp
  * (Eq. (10) with the sign carried by alpha), label +1 iff f(x) > 0 else -1.
  *
  * X_train    device, n x d row-major, dtype; alpha device, n values, dtype.
- * X_test     device, n_test x d row-major, dtype, n_test >= 1. Must be finite.
+ * X_test     device, n_test x d row-major, dtype, 1 <= n_test <= 2^22. Must be
+ *            finite.
  * scores_out device, n_test values, dtype.
  * labels_out device, n_test int32 values (+1/-1), may be NULL.
  * A NaN or an infinity in X_train or X_test returns LSSVM_ENONFINITE with
@@ -183,7 +187,7 @@ int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, i
  * One implicit product out = Q~ p of the reduced system (Eqs. (13), (16)),
  * the unit of work of each CG iteration.
  *
- * X     device, n x d row-major, dtype, n >= 2.
+ * X     device, n x d row-major, dtype, 2 <= n <= 2^22, 1 <= d <= 2^21.
  * p     device, N = n - 1 values, dtype. out device, N values, dtype.
  * Uses the lssvm_workspace_bytes(n, d, dtype) workspace.
  */

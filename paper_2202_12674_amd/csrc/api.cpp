@@ -53,6 +53,11 @@ namespace {
   } while (0)
 
 constexpr size_t kAlign = 256;
+// Supported sizes: the tile visit order takes n^2 / 8192 bytes (2 GiB at
+// n = 2^22) and packs tile indices in 16 bits; a panel's buffer span stays
+// below 4 GiB up to 2^21 features.
+constexpr int64_t kMaxPoints = int64_t(1) << 22;
+constexpr int64_t kMaxFeatures = int64_t(1) << 21;
 
 // LSSVM_LOG=1 in the environment: one stderr line per batch of CG iterations
 // and one per finished training (read once per process).
@@ -432,9 +437,7 @@ int check_sizes(int64_t n, int64_t d, int64_t min_n) {
   if (n < min_n) return fail(LSSVM_EINVAL, "n must be >= %lld (got %lld)", (long long)min_n,
                              (long long)n);
   if (d < 1) return fail(LSSVM_EINVAL, "d must be >= 1 (got %lld)", (long long)d);
-  // supported range: the tile visit order takes n^2 / 8192 bytes (2 GiB at
-  // n = 2^22), and the tile order packs tile indices in 16 bits
-  if (n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
+  if (n > kMaxPoints || d > kMaxFeatures)
     return fail(LSSVM_EINVAL, "problem too large (n=%lld, d=%lld)", (long long)n, (long long)d);
   return LSSVM_OK;
 }
@@ -1000,12 +1003,14 @@ int lssvm_cg_step_noalloc(int64_t N, double* x, double* r, double* d, const doub
 int64_t lssvm_host_contexts(void) { return g_pool_size.load(); }
 
 size_t lssvm_workspace_bytes(int64_t n, int64_t d, int32_t dtype) {
-  if (n < 1 || d < 1 || !valid_dtype(dtype)) return 0;
+  if (n < 1 || d < 1 || n > kMaxPoints || d > kMaxFeatures || !valid_dtype(dtype)) return 0;
   return dtype == LSSVM_F64 ? train_bytes<double>(n, d) : train_bytes<float>(n, d);
 }
 
 size_t lssvm_predict_workspace_bytes(int64_t n, int64_t n_test, int64_t d, int32_t dtype) {
-  if (n < 1 || n_test < 1 || d < 1 || !valid_dtype(dtype)) return 0;
+  if (n < 1 || n_test < 1 || d < 1 || n > kMaxPoints || n_test > kMaxPoints ||
+      d > kMaxFeatures || !valid_dtype(dtype))
+    return 0;
   return dtype == LSSVM_F64 ? predict_bytes<double>(n, n_test, d)
                             : predict_bytes<float>(n, n_test, d);
 }
@@ -1018,7 +1023,7 @@ int32_t lssvm_tile_size(int32_t dtype) {
 
 int lssvm_tile_plan(int64_t n, int64_t d, int32_t dtype, int32_t kernel, int64_t* plan) {
   clear_error();
-  if (n < 2 || d < 1 || n > (int64_t(1) << 22) || d > (int64_t(1) << 21))
+  if (n < 2 || d < 1 || n > kMaxPoints || d > kMaxFeatures)
     return fail(LSSVM_EINVAL, "tile_plan: need 2 <= n <= 2^22 and 1 <= d <= 2^21");
   if (kernel != LSSVM_LINEAR && kernel != LSSVM_POLY && kernel != LSSVM_RBF)
     return fail(LSSVM_EINVAL, "tile_plan: unknown kernel");
@@ -1077,7 +1082,7 @@ int lssvm_predict(const void* X_train, const void* alpha, double b, int64_t n, i
       return fail(LSSVM_EINVAL, "NULL array argument");
     if (!valid_dtype(dtype)) return fail(LSSVM_EINVAL, "unknown dtype %d", (int)dtype);
     LSSVM_TRY(check_sizes(n, d, 1));
-    if (n_test < 1 || n_test > (int64_t(1) << 22))
+    if (n_test < 1 || n_test > kMaxPoints)
       return fail(LSSVM_EINVAL, "n_test must be in [1, 2^22] (got %lld)", (long long)n_test);
     LSSVM_TRY(check_kernel_params(kernel, kp));
     if (!std::isfinite(b)) return fail(LSSVM_EINVAL, "b must be finite");

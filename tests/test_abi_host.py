@@ -50,6 +50,23 @@ def test_workspace_sizes():
     assert L.lssvm_tile_size(5) == 0
 
 
+def test_workspace_sizes_at_the_supported_limits():
+    # 2^22 points and 2^21 features are the largest sizes the entry points
+    # accept; beyond them the size queries answer 0 instead of a wrapped size
+    L = P.lib()
+    big, wide = 1 << 22, 1 << 21
+    for dt in (0, 1):
+        assert L.lssvm_workspace_bytes(big, 1, dt) > big * 8
+        assert L.lssvm_workspace_bytes(2, wide, dt) > 2 * wide * 4
+        assert L.lssvm_workspace_bytes(big + 1, 1, dt) == 0
+        assert L.lssvm_workspace_bytes(2, wide + 1, dt) == 0
+        assert L.lssvm_workspace_bytes(1 << 62, 1 << 40, dt) == 0
+        assert L.lssvm_predict_workspace_bytes(big, big, 1, dt) > 2 * big * 4
+        assert L.lssvm_predict_workspace_bytes(big + 1, 1, 1, dt) == 0
+        assert L.lssvm_predict_workspace_bytes(2, big + 1, 1, dt) == 0
+        assert L.lssvm_predict_workspace_bytes(2, 1, wide + 1, dt) == 0
+
+
 def test_workspace_grows_with_the_points_not_their_square():
     """A product's row sums take two 64-bit words per row (fixed-point
     accumulators), not a partial slot per tile column: at 2^20 points of 16
