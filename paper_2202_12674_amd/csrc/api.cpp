@@ -462,6 +462,19 @@ inline int64_t tile_split(const Geometry& g, int32_t kernel) {
   return kernel == LSSVM_LINEAR ? g.ksplit : 1;
 }
 
+// Feature split of the linear kernel's tiles in a fused iteration: a small
+// problem's few tiles take one CU each, and their matrix work is most of the
+// launch, so the split goes as far as one round of workgroups allows, down to
+// a single feature block per workgroup (which the two-stage loop of other
+// launches does not take).
+inline int64_t fused_split(const Geometry& g, int32_t kernel) {
+  if (kernel != LSSVM_LINEAR) return 1;
+  const int64_t nkb = g.d_pad / g.bk, W = tri_count(g.nT);
+  int64_t S = g.ksplit;
+  while (S < LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0 && W * 2 * S <= kResidentTiles) S *= 2;
+  return S;
+}
+
 template <typename T>
 TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params& kp,
                      int32_t kernel, const double* p) {
@@ -699,6 +712,7 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
         LSSVM_HIP(tm.start(s, k));
         TileArgs<T> a = sym_args<T>(g, w, kp, kernel, w.dir);
         a.stop = w.scal + S_STATUS + ST_DONE;
+        a.ksplit = fused_split(g, kernel);
         FusedCg f{w.ticket, rank_one(g, w, kernel, C, w.dir), w.qv, w.x, w.r, w.dir, w.scal,
                   w.hist, g.NP, g.N, k, g.NP + 1, par};
         LSSVM_HIP(launch_tiles_cg<T>(a, kernel, tri_count(g.nT) * a.ksplit, f, s));

@@ -800,11 +800,12 @@ __global__ __launch_bounds__(256) void k_finish_sum(const double* bpart, int64_t
 // k_cg_update and k_cg_direction do, for all rows at once. Each workgroup
 // fences its partial sums (device-scope release) before it takes a ticket;
 // the one that draws the last ticket fences again (acquire) and reads them
-// all. Rows r = tid + 256 k sit in registers (NP <= 1024 -> k < 4).
-template <typename T, int KER>
+// all. Rows r = tid + 256 k sit in registers (NP <= 1024 -> k < 4). ONE:
+// linear tiles split into single feature blocks (see tile_body).
+template <typename T, int KER, bool ONE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles_cg(
     TileArgs<T> a, FusedCg f) {
-  if (!tile_body<T, true, KER, kWhole>(a)) return;   // CG had already stopped
+  if (!tile_body<T, true, KER, kWhole, ONE>(a)) return;   // CG had already stopped
   __shared__ int last;
   __shared__ double sh[NT / 64];
   // Every wave releases its own writes (row sums, rank-one partials) at agent
@@ -1047,15 +1048,21 @@ hipError_t launch_tiles_cg(const TileArgs<T>& a0, int kernel, int64_t nwg, const
   TileArgs<T> a = a0;
   a.ntiles = nwg;
   a.tile_base = 0;
+  const bool one = kernel == KLIN && a.nkb == a.ksplit;   // a single feature block each
+  if (kernel != KLIN && a.ksplit != 1) return hipErrorInvalidValue;
   switch (kernel) {
     case KLIN:
-      hipLaunchKernelGGL((k_tiles_cg<T, KLIN>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      if (one)
+        hipLaunchKernelGGL((k_tiles_cg<T, KLIN, true>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      else
+        hipLaunchKernelGGL((k_tiles_cg<T, KLIN, false>), dim3((unsigned)nwg), dim3(256), 0, s, a,
+                           f);
       break;
     case KPOLY:
-      hipLaunchKernelGGL((k_tiles_cg<T, KPOLY>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      hipLaunchKernelGGL((k_tiles_cg<T, KPOLY, false>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
       break;
     default:
-      hipLaunchKernelGGL((k_tiles_cg<T, KRBF>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
+      hipLaunchKernelGGL((k_tiles_cg<T, KRBF, false>), dim3((unsigned)nwg), dim3(256), 0, s, a, f);
       break;
   }
   return hipGetLastError();

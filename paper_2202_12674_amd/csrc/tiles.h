@@ -261,10 +261,17 @@ __device__ const double kNeverStop = 0.0;
 // launch, one workgroup per tile, sums the parked splits in split order and
 // runs the epilogue.
 //
+// ONE: every workgroup of the launch contracts exactly one feature block
+// (a linear tile split into single blocks: the fused small-problem
+// iteration), so the block the prologue loads is the only one and the
+// two-stage loop is left out.
+//
 // The body returns false when the launch found CG already stopped (nothing
 // done), true otherwise.
-template <typename T, bool SYM, int KER, int PART>
+template <typename T, bool SYM, int KER, int PART, bool ONE = false>
 __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
+  static_assert(!ONE || (SYM && KER == KLIN && PART == kWhole),
+                "single-block workgroups: split linear tiles only");
   using MF = Mfma<T>;
   using C = TileCfg<T>;
   constexpr int BM = C::BM, BK = C::BK;
@@ -559,6 +566,9 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
   }
   vm_wait_all();
   __syncthreads();
+  if constexpr (ONE) {
+    compute(As0, Bs0);   // the epilogue touches none of the stages
+  } else {
   for (int64_t kb = 0; kb < nkb; kb += 2) {
     dload(kb + 1, As1, Bs1);
     __builtin_amdgcn_sched_barrier(0);
@@ -570,6 +580,7 @@ __device__ __forceinline__ bool tile_body(const TileArgs<T>& a) {
     compute(As1, Bs1);
     vm_wait_all();
     __syncthreads();
+  }
   }
   }
 
