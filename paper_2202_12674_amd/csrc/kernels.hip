@@ -44,11 +44,47 @@ __device__ inline double kernel_value64(double dot, double dist, double gamma, d
   }
 }
 
+// A commutative operation over the 64 lanes of a wave, every lane receiving
+// the result: the 8-lane half rows (DPP: half mirror, then the two quad
+// exchanges), the 16-lane rows (DPP rotate by 8), then row pairs and wave
+// halves (permlane swaps). Each step combines a lane's value with its
+// partner's, and both partners combine the same two values, so all lanes end
+// with the same bits. Cross-lane moves in registers: no LDS round trip per
+// step, as a shuffle would take.
+template <typename Op>
+__device__ inline double wave_reduce(double v, Op op) {
+  v = op(v, dpp_move<kDppRowHalfMirror>(v));
+  v = op(v, dpp_move<kDppQuadXor1>(v));
+  v = op(v, dpp_move<kDppQuadXor2>(v));
+  v = op(v, dpp_move<kDppRowRor8>(v));
+  {
+    const uint64_t u = as_u64(v);
+    const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)u, (uint32_t)u, false, false);
+    const auto hi =
+        __builtin_amdgcn_permlane16_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
+    v = op(as_f64(lo[0], hi[0]), as_f64(lo[1], hi[1]));   // rows 2k and 2k + 1
+  }
+  {
+    const uint64_t u = as_u64(v);
+    const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)u, (uint32_t)u, false, false);
+    const auto hi =
+        __builtin_amdgcn_permlane32_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
+    v = op(as_f64(lo[0], hi[0]), as_f64(lo[1], hi[1]));   // the two halves
+  }
+  return v;
+}
+struct AddOp {
+  __device__ double operator()(double a, double b) const { return a + b; }
+};
+struct MaxOp {
+  __device__ double operator()(double a, double b) const { return fmax(a, b); }
+};
+__device__ inline double wave_sum(double v) { return wave_reduce(v, AddOp{}); }
+
 // Block-wide sum of one double per thread; every thread gets the result.
 // Fixed reduction order, so every block that sums the same values agrees.
 __device__ inline double block_sum(double v, double* sh) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  v = wave_sum(v);
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   __syncthreads();
   if (l == 0) sh[w] = v;
@@ -85,8 +121,7 @@ __device__ inline double qtilde_row(const RankOne& c, const RankOneSums& r, int6
 // Block-wide maximum of one non-negative double per thread; every thread
 // gets it.
 __device__ inline double block_max(double v, double* sh) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  v = wave_reduce(v, MaxOp{});
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   __syncthreads();
   if (l == 0) sh[w] = v;
@@ -852,12 +887,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   // S and T of the rank-one terms (one reduction for both, each summed in
   // the order of block_sum)
-  double S = pS, Tq = pT;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    S += __shfl_xor(S, off);
-    Tq += __shfl_xor(Tq, off);
-  }
+  double S = wave_sum(pS), Tq = wave_sum(pT);
   {
     __shared__ double sh2[2][NT / 64];
     const int w = tid >> 6;
