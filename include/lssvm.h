@@ -288,10 +288,12 @@ int32_t lssvm_tile_size(int32_t dtype);
  *            kernels park their partial inner products and sum them in a
  *            fix-up launch;
  *   plan[2]  workgroups per such tile (plan[0] when plan[1] is 0).
- * Every split leaves an even number of feature blocks per workgroup. (The
- * one-launch CG iterations of small problems, n <= 1025 without a split
- * last round, may split the linear kernel's tiles further, down to a single
- * feature block per workgroup; plan[] describes every other product.)
+ * Every split leaves an even number of feature blocks per workgroup, except
+ * on small problems (n <= 1025 without a split last round, whose CG
+ * iterations are single launches): there the linear kernel's tiles split as
+ * far as one round of workgroups allows, down to one feature block each.
+ * Every product of a problem (CG iterations, residual recomputations,
+ * lssvm_matvec) uses the same plan.
  * Returns LSSVM_EINVAL (plan untouched) for n, d, dtype or kernel out of
  * range or a null plan. Informational. */
 int lssvm_tile_plan(int64_t n, int64_t d, int32_t dtype, int32_t kernel, int64_t* plan);

@@ -457,20 +457,21 @@ template <typename T> T rbf_scale(double gamma);
 template <> float rbf_scale<float>(double gamma) { return (float)(gamma * 1.4426950408889634); }
 template <> double rbf_scale<double>(double gamma) { return gamma; }
 
-// Workgroups per symmetric tile for this kernel function.
-inline int64_t tile_split(const Geometry& g, int32_t kernel) {
-  return kernel == LSSVM_LINEAR ? g.ksplit : 1;
-}
-
-// Feature split of the linear kernel's tiles in a fused iteration: a small
-// problem's few tiles take one CU each, and their matrix work is most of the
-// launch, so the split goes as far as one round of workgroups allows, down to
-// a single feature block per workgroup (which the two-stage loop of other
-// launches does not take).
-inline int64_t fused_split(const Geometry& g, int32_t kernel) {
+// Workgroups per tile of every product of n points (a training's CG
+// iterations, its residual recomputations, a warm start's and the true
+// residual's products, lssvm_matvec). On a small problem, whose iterations
+// are fused launches, the few tiles take one CU each and their matrix work
+// is most of the launch, so the linear kernel's split goes as far as one
+// round of workgroups allows, down to a single feature block per workgroup.
+// All products of a problem take the same split: each split rounds the
+// operator its own way (fp32 partial inner products), and a recomputed
+// residual from a differently rounded operator than the iterations' stalls
+// fp32 CG above its eps.
+inline int64_t product_split(const Geometry& g, int32_t kernel) {
   if (kernel != LSSVM_LINEAR) return 1;
-  const int64_t nkb = g.d_pad / g.bk, W = tri_count(g.nT);
   int64_t S = g.ksplit;
+  if (!fused_iteration(g, kernel)) return S;
+  const int64_t nkb = g.d_pad / g.bk, W = tri_count(g.nT);
   while (S < LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0 && W * 2 * S <= kResidentTiles) S *= 2;
   return S;
 }
@@ -494,7 +495,7 @@ TileArgs<T> sym_args(const Geometry& g, const TrainWs<T>& w, const lssvm_params&
   a.rbf_scale = rbf_scale<T>(kp.gamma);
   a.degree = kp.degree;
   a.nTc = g.nT;
-  a.ksplit = tile_split(g, kernel);
+  a.ksplit = product_split(g, kernel);
   a.order = LSSVM_TILE_GROUP > 0 ? w.order : nullptr;
   a.acc = w.acc;
   a.fx = w.scal + S_PMAX;      // [S_PMAX], [S_NMAX], [S_FIXSC]
@@ -712,7 +713,6 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
         LSSVM_HIP(tm.start(s, k));
         TileArgs<T> a = sym_args<T>(g, w, kp, kernel, w.dir);
         a.stop = w.scal + S_STATUS + ST_DONE;
-        a.ksplit = fused_split(g, kernel);
         FusedCg f{w.ticket, rank_one(g, w, kernel, C, w.dir), w.qv, w.x, w.r, w.dir, w.scal,
                   w.hist, g.NP, g.N, k, g.NP + 1, par};
         LSSVM_HIP(launch_tiles_cg<T>(a, kernel, tri_count(g.nT) * a.ksplit, f, s));
@@ -1045,7 +1045,7 @@ int lssvm_tile_plan(int64_t n, int64_t d, int32_t dtype, int32_t kernel, int64_t
   if (!plan) return fail(LSSVM_EINVAL, "tile_plan: null plan");
   const Geometry g = dtype == LSSVM_F64 ? geometry<double>(n, d) : geometry<float>(n, d);
   const bool lin = kernel == LSSVM_LINEAR;
-  plan[0] = tile_split(g, kernel);
+  plan[0] = product_split(g, kernel);
   plan[1] = lin ? g.lin_tail_q : g.tail_q;
   plan[2] = lin ? g.lin_tail_split : g.tail_split;
   if (plan[1] == 0) plan[2] = plan[0];

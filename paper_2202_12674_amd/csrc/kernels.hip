@@ -1041,7 +1041,10 @@ hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t nwg, hipStream_t s) {
     const dim3 grid((unsigned)std::min(kMaxTileGrid, nwg - base));
     switch (kernel) {
       case KLIN:
-        hipLaunchKernelGGL((k_tiles<T, SYM, KLIN, PART>), grid, dim3(256), 0, s, a);
+        if (SYM && PART == kWhole && a.nkb == a.ksplit)   // a single feature block each
+          hipLaunchKernelGGL((k_tiles_one<T>), grid, dim3(256), 0, s, a);
+        else
+          hipLaunchKernelGGL((k_tiles<T, SYM, KLIN, PART>), grid, dim3(256), 0, s, a);
         break;
       case KPOLY:
         hipLaunchKernelGGL((k_tiles<T, SYM, KPOLY, PART>), grid, dim3(256), 0, s, a);

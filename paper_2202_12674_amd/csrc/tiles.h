@@ -791,6 +791,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   tile_body<T, SYM, KER, PART>(a);
 }
 
+// Symmetric linear tiles split into single feature blocks (small problems:
+// the products outside the fused iteration use its split, so every product
+// of a training applies the same rounded operator).
+template <typename T>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_tiles_one(
+    TileArgs<T> a) {
+  tile_body<T, true, KLIN, kWhole, true>(a);
+}
+
 
 }  // namespace
 }  // namespace lssvm

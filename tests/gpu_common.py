@@ -76,9 +76,9 @@ def golden(name):
 # library's (workgroups per tile, tiles of the finer-split last round,
 # workgroups per such tile): splits without a tail, a tail over the split
 # full rounds, and a tail after unsplit ones (the 4096 x 1024 fp64 workload).
-SPLIT_SHAPES = [("f64", 600, 256, (8, 0, 8)), ("f64", 2000, 512, (4, 8, 16)),
+SPLIT_SHAPES = [("f64", 600, 256, (16, 0, 16)), ("f64", 2000, 512, (4, 8, 16)),
                 ("f64", 1000, 2048, (16, 4, 64)), ("f64", 3000, 256, (2, 44, 8)),
-                ("f64", 4096, 1024, (1, 16, 32)), ("f32", 1000, 256, (4, 0, 4)),
+                ("f64", 4096, 1024, (1, 16, 32)), ("f32", 1000, 256, (8, 0, 8)),
                 ("f32", 600, 1024, (16, 0, 16)), ("f32", 2000, 1024, (4, 8, 16)),
                 ("f32", 3000, 512, (2, 44, 8)), ("f32", 4096, 256, (1, 16, 4))]
 

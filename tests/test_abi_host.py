@@ -85,10 +85,14 @@ def test_workspace_grows_with_the_points_not_their_square():
 
 def test_tile_plan():
     """The launch plan of the implicit product: pinned for the five benchmark
-    workloads and the paper-sized linear problem, and for every shape split
-    widths that leave an even number of feature blocks per workgroup, a tail
-    exactly the tiles after the last full round, and at most one round of
-    workgroups in a tail launch; EINVAL (plan untouched) outside the range."""
+    workloads, the paper-sized linear problem and the smallest workload, and
+    for every shape split widths that leave an even number of feature blocks
+    per workgroup (on the small problems whose CG iterations are single
+    launches, n <= 1025 without a split last round, the linear kernel's tiles
+    split as far as one round of workgroups allows, down to one block each),
+    a tail exactly the tiles after the last full round, and at most one round
+    of workgroups in a tail launch; EINVAL (plan untouched) outside the
+    range."""
     L = P.lib()
     plan = (ctypes.c_int64 * 3)(-5, -5, -5)
     for args in [(1, 64, 0, 0), (256, 0, 0, 0), (256, 64, 9, 0), (256, 64, 0, 3),
@@ -101,7 +105,8 @@ def test_tile_plan():
             ("f64", "rbf", 16384, 2048): (1, 64, 8),
             ("f32", "poly", 32768, 4096): (1, 128, 4),
             ("f32", "rbf", 65536, 1024): (1, 0, 1),
-            ("f32", "rbf", 32768, 256): (1, 128, 4)}
+            ("f32", "rbf", 32768, 256): (1, 128, 4),
+            ("f64", "linear", 256, 64): (4, 0, 4)}
     for (dtype, kernel, n, d), want in pins.items():
         assert P.tile_plan(n, d, dtype, kernel) == want, (dtype, kernel, n, d)
     for dtype in ("f64", "f32"):
@@ -114,8 +119,15 @@ def test_tile_plan():
                     nT = -(-(n - 1) // 128)
                     W = nT * (nT + 1) // 2
                     where = (dtype, kernel, n, d, S, Q, T)
-                    assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, where
-                    assert T in (1, 2, 4, 8, 16, 32, 64) and nkb % (2 * T) == 0, where
+                    small = kernel == "linear" and n <= 1025 and Q == 0
+                    if small and S > 1 and nkb % (2 * S) != 0:
+                        # as split as the blocks and one round of workgroups allow
+                        assert nkb % S == 0 and W * S <= 512 and S <= 16, where
+                    else:
+                        assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, where
+                    if small:
+                        assert S == 16 or nkb % (2 * S) != 0 or W * 2 * S > 512, where
+                    assert T in (1, 2, 4, 8, 16, 32, 64) and (nkb % (2 * T) == 0 or T == S), where
                     if kernel != "linear":
                         assert S == 1, where
                     if Q == 0:

@@ -99,6 +99,24 @@ def test_train_small(torch_dev, dtype, kernel, n, d):
     check_train(torch, dev, cfg, ref, X, y, Xte, f_te, max_ties=len(Xte) if n == 2 else None)
 
 
+@pytest.mark.parametrize("n,d,C", [(962, 64, 22.3), (968, 76, 22.5), (606, 74, 10.3)])
+def test_train_fp32_linear_one_operator(torch_dev, n, d, C):
+    """Small fp32 linear trainings with d < n and large C (Q~ ill-conditioned):
+    fp32 CG reaches eps only if its residual recomputations apply the same
+    rounded operator as its iterations. These shapes stalled (or took 2-17x the
+    oracle's iterations) when the one-launch iterations split the tiles into
+    single feature blocks and the recomputations did not."""
+    torch, dev = torch_dev
+    cfg = small_cfg("linear", "f32", n, d, C=C)
+    X, y, Xte, _ = data_of(cfg)
+    ref = oracle_ref(cfg, X, y)
+    f_te = O.decision(X, ref.alpha, ref.b, Xte, spec_of(cfg))
+    sens = fp32_sensitivity(X, cfg)
+    tol = max(TOL_ALPHA["f32"], 0.1 * sens)
+    res = check_train(torch, dev, cfg, ref, X, y, Xte, f_te, alpha_tol=tol)
+    assert res.iterations <= ref.iterations + 20
+
+
 def test_train_residual_replacement(torch_dev):
     """C = 100 needs more than 50 iterations, so the residual is recomputed on the way."""
     torch, dev = torch_dev
