@@ -11,12 +11,15 @@ which.
 * ``bias_step_errors``: the bias step alone (Eqs. (11), (15)) on the GPU's own
   alpha~: alpha_m = -sum alpha~ and b = y_m + Q_mm sum alpha~ - q^T alpha~,
   each relative to its own size, against the oracle's recovery from the same
-  alpha~: the contract bar (plus, in fp32, the rounding of each alpha~_i to
-  fp32 on output, which the library's fp64 b does not see).
-* ``p9_check``: the CG iterate against the exact solution (Cholesky): for the
-  SPD reduced matrix lambda_min >= 1/C, so ||x - x*||_2 <= C ||rhs - Q~ x||_2
-  with the residual formed by the oracle's explicit fp64 Q~ (a rigorous bound,
-  no tolerance), and the alpha_m and b it implies.
+  alpha~: the contract bar, plus the fp64 rounding bound of the two sums
+  where the result is much smaller than its terms (plus, in fp32, the
+  rounding of each alpha~_i to fp32 on output, which the library's fp64 b
+  does not see).
+* ``p9_check``: the CG iterate against the exact solution: for the SPD
+  reduced matrix lambda_min >= 1/C, so ||x - x*||_2 <= C ||rhs - Q~ x||_2
+  with the residual formed by the oracle's explicit fp64 Q~, for the
+  iterate and for the Cholesky solution the check compares it with (a
+  rigorous bound, no tolerance), and the alpha_m and b it implies.
 * ``label_check``: labels equal to the oracle's except at points whose label
   the solution difference itself can flip: |f_ref| <= |f_mix - f_ref| + the
   prediction bar, where f_mix is the oracle's decision value for the GPU's
@@ -31,6 +34,7 @@ import oracle as O
 BAR_MV = {"f64": 1e-11, "f32": 1e-5}      # implicit product, max-norm relative
 BAR_SOL = {"f64": 1e-9, "f32": 1e-4}      # alpha and b
 U32 = 2.0 ** -24
+U64 = 2.0 ** -53
 
 
 def rel_to(delta, ref, scale):
@@ -73,7 +77,11 @@ def bias_step_errors(alpha, b, y, q, Qmm, dtype):
     """The bias step on the GPU's own alpha~: (error of alpha_m, its tolerance,
     error of b, its tolerance), errors relative to |alpha_m| and |b|.
 
-    Tolerance: the contract bar, plus in fp32 the effect of rounding each
+    Tolerance: the contract bar, plus the rounding of the two sums themselves
+    where alpha_m or b is much smaller than their terms (both sides sum in
+    fp64: the library a strided sum of ceil(N / 1024) terms per thread and a
+    tree, the oracle pairwise; together below (ceil(N / 1024) + 40) u64 times
+    the sum of the terms' magnitudes), plus in fp32 the effect of rounding each
     alpha~_i to fp32 on output (|delta alpha~_i| <= 2^-24 |alpha~_i|; the
     library forms alpha_m and b from its fp64 iterate): sum |alpha~_i| u32 for
     alpha_m (and u32 |alpha_m| for its own rounding), sum |Q_mm - q_i|
@@ -86,6 +94,11 @@ def bias_step_errors(alpha, b, y, q, Qmm, dtype):
     e_am = rel_to(alpha[-1] - ref_alpha[-1], ref_alpha[-1], sa)
     e_b = rel_to(b - ref_b, ref_b, 1.0)
     tol_am, tol_b = bar, bar
+    n_sum = (-(-at.shape[0] // 1024) + 40) * U64
+    den_am64 = abs(ref_alpha[-1]) if abs(ref_alpha[-1]) > 0 else sa
+    den_b64 = abs(ref_b) if abs(ref_b) > 0 else 1.0
+    tol_am += n_sum * float(at.sum()) / den_am64
+    tol_b += n_sum * (abs(Qmm) * float(at.sum()) + float(np.abs(q) @ at)) / den_b64
     if dtype == "f32":
         den_am = abs(ref_alpha[-1]) if abs(ref_alpha[-1]) > 1e-6 * sa else sa
         den_b = abs(ref_b) if abs(ref_b) > 1e-6 else 1.0
@@ -95,19 +108,23 @@ def bias_step_errors(alpha, b, y, q, Qmm, dtype):
 
 
 def p9_check(alpha, b, Qt, q, Qmm, rhs, C, x_exact, b_exact):
-    """Rigorous distance of the GPU's solution to the exact one (Cholesky).
+    """Rigorous distance of the GPU's solution to the exact one.
 
     ||alpha~ - x*||_2 <= C ||rhs - Q~ alpha~||_2 because lambda_min(Q~) >= 1/C
-    (Q~ = P^T Q P with Q >= I/C and P^T P = I + 1 1^T >= I). It implies
+    (Q~ = P^T Q P with Q >= I/C and P^T P = I + 1 1^T >= I). The reference
+    x_exact is the Cholesky solution, itself within C ||rhs - Q~ x_exact||_2 of
+    x* by the same bound (which matters where Q~ is ill-conditioned), so the
+    distance between the two is below the sum D of both bounds. It implies
     |alpha_m - alpha_m*| <= sqrt(N) D and |b - b*| <= (|Q_mm| sqrt(N) + ||q||_2) D
-    with D that bound (Eqs. (11), (15) are linear in alpha~). Returns the
-    distances, their bounds and the relative residual ||r|| / ||rhs||."""
+    (Eqs. (11), (15) are linear in alpha~). Returns the distances, their
+    bounds and the relative residual ||r|| / ||rhs||."""
     alpha = np.asarray(alpha, dtype=np.float64)
     at = alpha[:-1]
     N = at.shape[0]
     r = rhs - Qt @ at
-    D = C * float(np.linalg.norm(r))
-    slack = 1e-12 * (float(np.linalg.norm(x_exact)) + 1.0)   # rounding of the two solves
+    r_exact = rhs - Qt @ x_exact[:N]
+    D = C * (float(np.linalg.norm(r)) + float(np.linalg.norm(r_exact)))
+    slack = 1e-12 * (float(np.linalg.norm(x_exact)) + 1.0)   # rounding of the residuals
     dist = float(np.linalg.norm(at - x_exact[:N]))
     d_am = abs(alpha[-1] - (-float(x_exact[:N].sum())))
     d_b = abs(b - b_exact)
