@@ -472,7 +472,11 @@ inline int64_t product_split(const Geometry& g, int32_t kernel) {
   int64_t S = g.ksplit;
   if (!fused_iteration(g, kernel)) return S;
   const int64_t nkb = g.d_pad / g.bk, W = tri_count(g.nT);
-  while (S < LSSVM_LINEAR_SPLIT_MAX && nkb % (2 * S) == 0 && W * 2 * S <= kResidentTiles) S *= 2;
+  // double while every workgroup keeps an even block count (the two-stage
+  // loop) or gets exactly one (the single-block variant)
+  while (S < LSSVM_LINEAR_SPLIT_MAX && W * 2 * S <= kResidentTiles &&
+         (nkb % (4 * S) == 0 || nkb == 2 * S))
+    S *= 2;
   return S;
 }
 

@@ -1033,8 +1033,18 @@ hipError_t launch_norms_q(const T* Xt, int64_t ld, int64_t d_pad, int64_t m, int
 // items one dispatch can count; a multiple of 8, so every chunk starts on XCD 0.
 constexpr int64_t kMaxTileGrid = int64_t(1) << 23;
 
+// Feature blocks per workgroup: even (the two-stage loop runs them in pairs)
+// or exactly one (the single-block variant).
+template <typename T>
+inline bool blocks_ok(const TileArgs<T>& a, int64_t split) {
+  if (split < 1 || a.nkb % split != 0) return false;
+  const int64_t per = a.nkb / split;
+  return per % 2 == 0 || per == 1;
+}
+
 template <typename T, bool SYM, int PART>
 hipError_t launch_tiles(TileArgs<T> a, int kernel, int64_t nwg, hipStream_t s) {
+  if (SYM && PART != kFixup && !blocks_ok(a, a.ksplit)) return hipErrorInvalidValue;
   a.ntiles = nwg;
   for (int64_t base = 0; base < nwg; base += kMaxTileGrid) {
     a.tile_base = base;
@@ -1082,7 +1092,7 @@ hipError_t launch_tiles_cg(const TileArgs<T>& a0, int kernel, int64_t nwg, const
   a.ntiles = nwg;
   a.tile_base = 0;
   const bool one = kernel == KLIN && a.nkb == a.ksplit;   // a single feature block each
-  if (kernel != KLIN && a.ksplit != 1) return hipErrorInvalidValue;
+  if ((kernel != KLIN && a.ksplit != 1) || !blocks_ok(a, a.ksplit)) return hipErrorInvalidValue;
   switch (kernel) {
     case KLIN:
       if (one)

@@ -120,14 +120,16 @@ def test_tile_plan():
                     W = nT * (nT + 1) // 2
                     where = (dtype, kernel, n, d, S, Q, T)
                     small = kernel == "linear" and n <= 1025 and Q == 0
-                    if small and S > 1 and nkb % (2 * S) != 0:
-                        # as split as the blocks and one round of workgroups allow
-                        assert nkb % S == 0 and W * S <= 512 and S <= 16, where
+                    assert S in (1, 2, 4, 8, 16), where
+                    if small and S == nkb:
+                        assert S > 1 and W * S <= 512, where   # one feature block each
                     else:
-                        assert S in (1, 2, 4, 8, 16) and nkb % (2 * S) == 0, where
-                    if small:
-                        assert S == 16 or nkb % (2 * S) != 0 or W * 2 * S > 512, where
-                    assert T in (1, 2, 4, 8, 16, 32, 64) and (nkb % (2 * T) == 0 or T == S), where
+                        assert nkb % (2 * S) == 0, where       # an even count each
+                    if small and S < nkb:
+                        # as split as the blocks and one round of workgroups allow
+                        assert (S == 16 or W * 2 * S > 512
+                                or (nkb % (4 * S) != 0 and nkb != 2 * S)), where
+                    assert T in (1, 2, 4, 8, 16, 32, 64) and (nkb % (2 * T) == 0 or T == S == nkb), where
                     if kernel != "linear":
                         assert S == 1, where
                     if Q == 0:
