@@ -138,8 +138,8 @@ inline int64_t linear_tail_split(int64_t Q, int64_t S, int64_t nkb) {
 // the Q tiles left for a last partial round run as the launch's trailing
 // workgroups, split T >= S ways (the feature shares add into the row sums
 // like any split's, so no fixup is needed), which takes 1/T of a tile plus
-// the fixed cost. S (and T) halve the block count, which must stay even. A problem of
-// one round or less keeps its tiles in one launch.
+// the fixed cost. S (and T) halve the block count, which must stay even. A
+// problem of one round or less keeps its tiles in one launch.
 inline void linear_plan(int64_t nT, int64_t nkb, int64_t* split, int64_t* q, int64_t* tail_split) {
   const int64_t W = tri_count(nT);
   const double f = 2.0 / (double)nkb;

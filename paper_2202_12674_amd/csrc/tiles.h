@@ -262,9 +262,8 @@ __device__ const double kNeverStop = 0.0;
 // runs the epilogue.
 //
 // ONE: every workgroup of the launch contracts exactly one feature block
-// (a linear tile split into single blocks: the fused small-problem
-// iteration), so the block the prologue loads is the only one and the
-// two-stage loop is left out.
+// (a small problem's linear tiles split into single blocks), so the block
+// the prologue loads is the only one and the two-stage loop is left out.
 //
 // The body returns false when the launch found CG already stopped (nothing
 // done), true otherwise.
