@@ -100,7 +100,9 @@ struct Geometry {
 // Small problems run each CG iteration (except the residual recomputations)
 // as one launch: the product's tiles and, in the last workgroup, the vector
 // work (launch_tiles_cg). Their iterations are launch-bound: four dependent
-// launches of a few microseconds each against a product of ~10 us.
+// launches of a few microseconds each against a product of ~10 us. (At 4096
+// points the same fusion cost more than it saved: the release and ticket of
+// each of ~1000 workgroups made the launch ~50 us longer than the product.)
 inline bool fused_iteration(const Geometry& g, int32_t kernel) {
   const bool one_launch = kernel == LSSVM_LINEAR ? g.lin_tail_q == 0 : g.tail_q == 0;
   return LSSVM_FUSED_SMALL && g.NP <= kFusedMaxNP && one_launch;
@@ -555,21 +557,25 @@ RankOne rank_one(const Geometry& g, const TrainWs<T>& w, int32_t kernel, double 
 // The tile launches of one product: all tiles whole (the linear kernel's
 // split tiles included), or the full rounds whole and the tail split, parked
 // and fixed up.
+// The one launch of a linear product: its workgroup count, with a's fields
+// for the finer-split last round set. Feature splits add up, so the last
+// round only splits finer, as the launch's trailing workgroups: they start
+// as the whole tiles finish, with no second launch to wait for.
+template <typename T>
+int64_t linear_launch(const Geometry& g, TileArgs<T>& a) {
+  const int64_t F = tri_count(g.nT) - g.lin_tail_q;
+  if (g.lin_tail_q == 0) return F * a.ksplit;
+  a.tail_slot = F * a.ksplit;
+  a.tail_split = g.lin_tail_split;
+  a.tail_tile = F;
+  return F * a.ksplit + g.lin_tail_q * g.lin_tail_split;
+}
+
 template <typename T>
 hipError_t launch_product(const Geometry& g, TileArgs<T> a, int32_t kernel, T* gpart,
                           hipStream_t s) {
   const int64_t W = tri_count(g.nT);
-  if (kernel == LSSVM_LINEAR) {   // feature splits add up: the tail only splits finer
-    const int64_t F = W - g.lin_tail_q;
-    if (g.lin_tail_q == 0) return launch_tiles_sym<T>(a, kernel, kWhole, F * a.ksplit, s);
-    // the finer-split last round as the launch's trailing workgroups: they
-    // start as the whole tiles finish, with no second launch to wait for
-    a.tail_slot = F * a.ksplit;
-    a.tail_split = g.lin_tail_split;
-    a.tail_tile = F;
-    return launch_tiles_sym<T>(a, kernel, kWhole,
-                               F * a.ksplit + g.lin_tail_q * g.lin_tail_split, s);
-  }
+  if (kernel == LSSVM_LINEAR) return launch_tiles_sym<T>(a, kernel, kWhole, linear_launch(g, a), s);
   if (g.tail_q == 0) return launch_tiles_sym<T>(a, kernel, kWhole, W, s);
   const int64_t F = W - g.tail_q;
   hipError_t e = launch_tiles_sym<T>(a, kernel, kWhole, F, s);
@@ -719,7 +725,8 @@ int train_impl(const T* X, const T* y, int64_t n, int64_t d, int32_t kernel,
         a.stop = w.scal + S_STATUS + ST_DONE;
         FusedCg f{w.ticket, rank_one(g, w, kernel, C, w.dir), w.qv, w.x, w.r, w.dir, w.scal,
                   w.hist, g.NP, g.N, k, g.NP + 1, par};
-        LSSVM_HIP(launch_tiles_cg<T>(a, kernel, tri_count(g.nT) * a.ksplit, f, s));
+        const int64_t nwg = kernel == LSSVM_LINEAR ? linear_launch(g, a) : tri_count(g.nT);
+        LSSVM_HIP(launch_tiles_cg<T>(a, kernel, nwg, f, s));
         LSSVM_HIP(tm.stop(s));
         continue;
       }
