@@ -21,7 +21,7 @@ TOL_ALPHA = BAR_SOL
 
 __all__ = ["GOLDEN", "TOL_MV", "TOL_ALPHA", "BAR_MV", "BAR_SOL", "rel_err", "log", "spec_of",
            "kw_of", "small_cfg", "data_of", "to_dev", "golden", "golden_tight", "SPLIT_SHAPES",
-           "TAIL_SHAPES", "random_cases", "random_large_cases",
+           "TAIL_SHAPES", "random_cases", "random_large_cases", "random_param_cases",
            "fp32_sensitivity", "OracleRef", "oracle_ref", "check_train", "labels_match"]
 
 
@@ -111,6 +111,26 @@ def random_large_cases(count=16, seed=11):
         d = int(np.exp(rng.uniform(np.log(100), np.log(5000))))
         kernel = ["linear", "poly", "rbf"][rng.integers(3)]
         dtype = ["f64", "f32"][rng.integers(2)]
+        C = float(10 ** rng.uniform(-2, 2))
+        kp = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=float(rng.choice([0.0, 1.0])),
+                                       degree=int(rng.integers(1, 5))),
+                  rbf=dict(gamma=float(10 ** rng.uniform(-1, 0.5)) / d))[kernel]
+        out.append((kernel, dtype, n, d, C, kp))
+    return out
+
+
+def random_param_cases(count=48, seed=31337):
+    """Seeded small shapes (2..2500 points log-uniform, 1..1500 features) with
+    random kernel parameters and C from 0.01 to 100: every split of the
+    linear kernel's small problems (down to one feature block per workgroup)
+    and every kernel function's epilogue on ragged tiles."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(count):
+        n = max(2, int(np.exp(rng.uniform(np.log(2), np.log(2500)))))
+        d = int(np.exp(rng.uniform(0, np.log(1500))))
+        kernel = ["linear", "poly", "rbf"][k % 3]
+        dtype = ["f64", "f32"][(k // 3) % 2]
         C = float(10 ** rng.uniform(-2, 2))
         kp = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=float(rng.choice([0.0, 1.0])),
                                        degree=int(rng.integers(1, 5))),

@@ -12,7 +12,8 @@ import oracle as O
 import synthdata as S
 from gpu_common import (GOLDEN, TOL_ALPHA, TOL_MV, SPLIT_SHAPES, TAIL_SHAPES, check_train,  # noqa: F401
                         data_of, golden, golden_tight, kw_of, labels_match, log, oracle_ref,
-                        random_cases, random_large_cases, rel_err, small_cfg, spec_of,
+                        random_cases, random_large_cases, random_param_cases, rel_err, small_cfg,
+                        spec_of,
                         to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -85,6 +86,24 @@ def test_matvec_random_shapes(torch_dev, kernel, dtype, n, d, C):
     out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=C, **kw_of(cfg))
     Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), C)
     assert rel_err(out.cpu().numpy(), Qt @ p.astype(np.float64)) <= TOL_MV[dtype]
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d,C,kp", random_param_cases())
+def test_matvec_random_params(torch_dev, kernel, dtype, n, d, C, kp):
+    """Small random shapes with random kernel parameters and C: the full
+    product against the oracle's explicit Q~ p at the bar."""
+    torch, dev = torch_dev
+    import paper_2202_12674_amd as P
+    cfg = S.Config(f"{kernel}_{dtype}_{n}x{d}", dtype, kernel, n, d, mu=1.0, inf_frac=0.5,
+                   flip_frac=0.05, C=C, eps=1e-8, **kp)
+    X, _, _ = S.make_train(cfg)
+    p = S.probe_vector(n - 1, cfg.np_dtype, seed=n + d)
+    out = P.matvec(to_dev(torch, dev, X), to_dev(torch, dev, p), C=C, **kw_of(cfg)).cpu().numpy()
+    Qt, _, _ = O.reduced_matrix(X, spec_of(cfg), C)
+    err = rel_err(out, Qt @ p.astype(np.float64))
+    log(f"matvec random params {cfg.name} C={C:.3g} {kp} plan {P.tile_plan(n, d, dtype, kernel)}:"
+        f" {err:.2e}")
+    assert err <= TOL_MV[dtype]
 
 
 @pytest.mark.parametrize("kernel,dtype,n,d,C,kp", random_large_cases())
