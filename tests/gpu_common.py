@@ -21,7 +21,7 @@ TOL_ALPHA = BAR_SOL
 
 __all__ = ["GOLDEN", "TOL_MV", "TOL_ALPHA", "BAR_MV", "BAR_SOL", "rel_err", "log", "spec_of",
            "kw_of", "small_cfg", "data_of", "to_dev", "golden", "golden_tight", "SPLIT_SHAPES",
-           "TAIL_SHAPES", "random_cases", "random_large_cases", "random_param_cases",
+           "TAIL_SHAPES", "random_cases", "random_large_cases", "random_param_cases", "random_param_train_cases",
            "fp32_sensitivity", "OracleRef", "oracle_ref", "check_train", "labels_match"]
 
 
@@ -132,6 +132,25 @@ def random_param_cases(count=48, seed=31337):
         kernel = ["linear", "poly", "rbf"][k % 3]
         dtype = ["f64", "f32"][(k // 3) % 2]
         C = float(10 ** rng.uniform(-2, 2))
+        kp = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=float(rng.choice([0.0, 1.0])),
+                                       degree=int(rng.integers(1, 5))),
+                  rbf=dict(gamma=float(10 ** rng.uniform(-1, 0.5)) / d))[kernel]
+        out.append((kernel, dtype, n, d, C, kp))
+    return out
+
+
+def random_param_train_cases(count=12, seed=4711):
+    """Seeded trainings of 50..1500 points and 2..600 features with random
+    kernel parameters (polynomial degree 1..4, coef0 0 or 1, RBF gamma 0.1/d
+    to 3/d) and C from 0.1 to 10."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(count):
+        n = int(np.exp(rng.uniform(np.log(50), np.log(1500))))
+        d = int(np.exp(rng.uniform(np.log(2), np.log(600))))
+        kernel = ["linear", "poly", "rbf"][k % 3]
+        dtype = ["f64", "f32"][(k // 3) % 2]
+        C = float(10 ** rng.uniform(-1, 1))
         kp = dict(linear={}, poly=dict(gamma=1.0 / d, coef0=float(rng.choice([0.0, 1.0])),
                                        degree=int(rng.integers(1, 5))),
                   rbf=dict(gamma=float(10 ** rng.uniform(-1, 0.5)) / d))[kernel]

@@ -17,7 +17,8 @@ import synthdata as S
 from gpu_common import (GOLDEN, TOL_ALPHA, TOL_MV, SPLIT_SHAPES, TAIL_SHAPES, check_train,  # noqa: F401
                         fp32_sensitivity,
                         data_of, golden, golden_tight, kw_of, labels_match, log, oracle_ref,
-                        random_cases, random_large_cases, rel_err, small_cfg, spec_of,
+                        random_cases, random_large_cases, random_param_train_cases, rel_err,
+                        small_cfg, spec_of,
                         to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -81,6 +82,22 @@ def test_train_random_shapes(torch_dev, kernel, dtype, n, d, C):
     sens = fp32_sensitivity(X, cfg) if dtype == "f32" else 0.0
     tol = max(TOL_ALPHA[dtype], 0.1 * sens)
     log(f"  {cfg.name} C={C}: kappa u32 <= {sens:.1e}, alpha~ tolerance {tol:.1e}")
+    check_train(torch, dev, cfg, ref, X, y, Xte, f_te, alpha_tol=tol)
+
+
+@pytest.mark.parametrize("kernel,dtype,n,d,C,kp", random_param_train_cases())
+def test_train_random_params(torch_dev, kernel, dtype, n, d, C, kp):
+    """Every rule of check_train on trainings with random kernel parameters,
+    the fp32 alpha~ tolerance as in test_train_random_shapes."""
+    torch, dev = torch_dev
+    cfg = S.Config(f"{kernel}_{dtype}_{n}x{d}", dtype, kernel, n, d, mu=1.0, inf_frac=0.5,
+                   flip_frac=0.05, C=C, eps=1e-10 if dtype == "f64" else 1e-5, **kp)
+    X, y, Xte, _ = data_of(cfg)
+    ref = oracle_ref(cfg, X, y)
+    f_te = O.decision(X, ref.alpha, ref.b, Xte, spec_of(cfg))
+    sens = fp32_sensitivity(X, cfg) if dtype == "f32" else 0.0
+    tol = max(TOL_ALPHA[dtype], 0.1 * sens)
+    log(f"  {cfg.name} C={C:.3g} {kp}: kappa u32 <= {sens:.1e}, alpha~ tolerance {tol:.1e}")
     check_train(torch, dev, cfg, ref, X, y, Xte, f_te, alpha_tol=tol)
 
 
